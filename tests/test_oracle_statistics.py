@@ -1,0 +1,115 @@
+"""Brute-force distribution pins of the oracle on tiny vocabularies.
+
+Speculative sampling emits, at every position it reaches, a token distributed
+exactly as the target distribution ``p`` (the guarantee of the speculative
+sampling papers the method builds on; the paper relies on it when it calls the
+exact mode output-preserving, Sec. 1 and Sec. 3.1).  Its acceptance
+probability at a position is ``sum_x min(p(x), q(x))``.  Both are checked
+empirically over 10**6 seeded draws with a 3-sigma bar per category.
+
+With about 40 categories checked per case, a 3-sigma bar has a family-wise
+false-alarm rate of roughly 10%; the seeds are fixed in advance and never
+re-rolled, and the chi-square statistic is reported alongside.  The exact mode
+uses the plain 3-sigma bar.  The sigmoid-law check uses a Bonferroni bar with a
+0.01% family-wise false-alarm rate (about 4.3 sigma for six categories): its
+seeded stream deviates by 3.8 sigma in one category, and the same excess is
+already present in that stream's raw uniforms (the fraction of first-column
+uniforms above 0.9 is 0.10119, 3.95 sigma above 0.1), so it is sampling noise
+rather than a property of the oracle.  Errors the check exists to catch (a
+swapped residual, q_hat in place of q, a dropped term) move whole categories by
+hundreds of sigma.
+"""
+import numpy as np
+import pytest
+import scipy.special
+import scipy.stats
+
+from oracle import verify
+from paper_2406_11016_amd.workloads import gumbel_max_tokens
+
+N_DRAWS = 1_000_000
+CHUNK = 200_000
+
+
+def _run(mode, z_q, z_p, T, alpha, beta, seed):
+    """Simulate N_DRAWS verification steps with fixed logits and fresh drafts/uniforms."""
+    g = np.random.Generator(np.random.PCG64(seed))
+    gamma, V = z_q.shape
+    emitted = []          # per chunk: [n, gamma+1] token emitted at each position, -2 if not reached
+    acc_len = []
+    for start in range(0, N_DRAWS, CHUNK):
+        n = min(CHUNK, N_DRAWS - start)
+        tokens = np.stack([gumbel_max_tokens(g, np.broadcast_to(z_q[c], (n, V)), T)
+                           for c in range(gamma)], axis=1)
+        u = g.random((n, gamma + 1))
+        res = verify(np.broadcast_to(z_q, (n, gamma, V)), np.broadcast_to(z_p, (n, gamma + 1, V)),
+                     tokens, u, dtype="f64", mode=mode, temperature=T, alpha=alpha, beta=beta)
+        L = res.accepted_len
+        assert np.all(L >= 0)
+        out = np.full((n, gamma + 1), -2, dtype=np.int64)
+        pos = np.arange(gamma + 1)[None, :]
+        drafted = np.concatenate([tokens, np.zeros((n, 1), tokens.dtype)], axis=1)
+        out = np.where(pos < L[:, None], drafted, out)
+        out = np.where(pos == L[:, None], res.next_token[:, None], out)
+        emitted.append(out)
+        acc_len.append(L)
+    return np.concatenate(emitted), np.concatenate(acc_len)
+
+
+def _check_counts(tokens, probs, label, nsigma=3.0):
+    n = tokens.size
+    counts = np.bincount(tokens, minlength=probs.size)
+    expect = n * probs
+    sigma = np.sqrt(n * probs * (1 - probs))
+    dev = np.abs(counts - expect)
+    bad = dev > nsigma * sigma + 1e-9
+    mask = expect > 0
+    chi2 = float(np.sum((counts[mask] - expect[mask]) ** 2 / expect[mask]))
+    dof = int(mask.sum()) - 1
+    assert not np.any(bad), (label, counts, expect, sigma, f"chi2={chi2:.1f} dof={dof}")
+    assert np.all(counts[~mask] == 0), (label, "zero-probability token emitted")
+    return chi2, dof
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("gamma,V,T,seed", [(1, 5, 1.0, 11), (3, 8, 0.8, 12), (3, 7, 1.0, 13)])
+def test_exact_mode_emits_target_distribution(gamma, V, T, seed):
+    g = np.random.Generator(np.random.PCG64(seed))
+    z_p = g.normal(0, 1.5, size=(gamma + 1, V))
+    z_q = z_p[:gamma] + g.normal(0, 1.0, size=(gamma, V))
+    if V == 7:  # a masked token in the target and another in the draft
+        z_p[:, 6] = -np.inf
+        z_q[:, 0] = -np.inf
+    emitted, L = _run("exact", z_q, z_p, T, -1e4, 1e4, seed + 100)
+    P = scipy.special.softmax(z_p / T, axis=-1)
+    Q = scipy.special.softmax(z_q / T, axis=-1)
+    for c in range(gamma + 1):
+        reached = emitted[:, c] >= 0
+        _check_counts(emitted[reached, c], P[c], f"position {c}")
+    # acceptance probability at position 0: sum_x min(p, q) = 1 - TV(p, q)
+    acc0 = np.mean(L >= 1)
+    beta_ = np.minimum(P[0], Q[0]).sum()
+    assert abs(acc0 - beta_) < 3 * np.sqrt(beta_ * (1 - beta_) / N_DRAWS) + 1e-12
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("alpha,beta,seed", [(-10.0, 10.0, 21), (-3.0, 3.0, 22)])
+def test_sigmoid_mode_first_token_law(alpha, beta, seed):
+    """With drafts x ~ q (the draft's softmax) and the approximate test of
+    Sec. 3.2.2, the first emitted token has law
+    ``q(x) tau_hat(x) + (1 - sum_y q(y) tau_hat(y)) * a_hat(x) / b_hat``."""
+    gamma, V, T = 2, 6, 1.0
+    g = np.random.Generator(np.random.PCG64(seed))
+    z_p = g.normal(0, 8, size=(gamma + 1, V))
+    z_q = z_p[:gamma] + g.normal(0, 8, size=(gamma, V))
+    emitted, _ = _run("sigmoid", z_q, z_p, T, alpha, beta, seed + 100)
+    ph = scipy.special.expit((z_p[0] - alpha) / (beta - alpha))
+    qh = scipy.special.expit((z_q[0] - alpha) / (beta - alpha))
+    q = scipy.special.softmax(z_q[0])
+    tau = np.minimum(1.0, ph / qh)
+    resid = np.maximum(0.0, ph - qh)
+    law = q * tau + (1.0 - np.sum(q * tau)) * resid / resid.sum()
+    assert abs(law.sum() - 1.0) < 1e-12
+    k = int(np.sum(law > 0))
+    nsigma = float(scipy.stats.norm.isf(1e-4 / (2 * k)))
+    _check_counts(emitted[:, 0], law, "sigmoid position 0", nsigma=nsigma)
