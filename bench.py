@@ -1,0 +1,185 @@
+"""Throughput of the fused speculative-sampling verification step on one GPU.
+
+One step is one complete ``spec_verify_*`` call over one batch of synthetic
+logits already resident in device memory.  Prints one JSON line with
+verify-steps/s, the roofline position of the step (algorithmic HBM bytes per
+step / measured step time, against MI355X's 8 TB/s), and the CPU oracle timed
+on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "verify-steps/sec and achieved HBM GB/s (fraction of peak) at 1 MI355X"
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(w) -> int:
+    """Bytes a step must move at least: exact mode reads every logit once
+    (B (2 gamma + 1) V s); sigmoid mode reads the drafted-token logits and the
+    row(s) the next token is drawn from (counted as the two-row residual case).
+    Plus tokens, uniforms and the two outputs."""
+    from paper_2406_11016_amd.workloads import BYTES_PER_LOGIT
+    s = BYTES_PER_LOGIT[w.dtype]
+    small = w.batch * (w.gamma * 4 + (w.gamma + 1) * 4 + 2 * 4)
+    if w.mode == "exact":
+        return w.batch * (2 * w.gamma + 1) * w.vocab * s + small
+    return w.batch * (2 * w.gamma * s + 2 * w.vocab * s) + small
+
+
+def cpu_baseline(w, x, min_seconds: float):
+    """The oracle as it stands, timed on a bounded sample of the same inputs."""
+    import numpy as np
+
+    import oracle
+    nb = min(w.batch, 16)
+    sl = slice(0, nb)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        with np.errstate(all="ignore"):
+            oracle.verify(x.draft[sl], x.target[sl], x.tokens[sl], x.uniforms[sl], dtype=x.dtype, mode=x.mode,
+                          temperature=x.temperature, alpha=x.alpha, beta=x.beta)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            break
+    steps_per_s = reps * nb / w.batch / el
+    return {"value": steps_per_s, "unit": "verify-steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"float64 NumPy oracle on batch elements 0..{nb - 1} of {w.batch} "
+                      f"({reps} repetitions, {el:.1f} s, single thread), scaled to whole steps"}
+
+
+def copy_calibration(nbytes: int, reps: int) -> None:
+    """A plain device-to-device copy of known size, for scaling HBM counters."""
+    import torch
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--rotate-mb", type=float, default=768.0,
+                    help="device copies of the inputs are rotated so that at least this many MB are cycled "
+                         "(defeats the 256 MB last-level cache)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=float, default=0.0,
+                    help="only run a plain copy of this size (for counter calibration) and exit")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(batch elements are independent, so N GPUs would each run this step on B/N)", file=sys.stderr)
+        return 2
+    if args.copy_calibration_mb > 0:
+        copy_calibration(int(args.copy_calibration_mb * 1e6), 20)
+        return 0
+
+    import torch
+
+    from paper_2406_11016_amd import binding
+    from paper_2406_11016_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        return 1
+    w = W.WORKLOADS[args.workload or W.HEADLINE]
+    dev = torch.device("cuda:0")
+    binding.load_library()
+
+    log(f"generating {w.name} ({w.logit_bytes / 1e6:.1f} MB of logits)")
+    t0 = time.perf_counter()
+    x = W.generate(w)
+    log(f"generated in {time.perf_counter() - t0:.1f} s; uploading")
+    d0, t0_, tok, uni = binding.to_device(x, dev)
+    nrot = max(1, int((args.rotate_mb * 1e6 + w.logit_bytes - 1) // w.logit_bytes))
+    sets = [(d0, t0_)] + [(d0.clone(), t0_.clone()) for _ in range(nrot - 1)]
+    acc = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    nxt = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    ws = binding.new_workspace(w.batch, w.gamma, w.vocab, d0.dtype, dev)
+    torch.cuda.synchronize(dev)
+
+    def step(i):
+        d, t = sets[i % nrot]
+        binding.verify(d, t, tok, uni, mode=w.mode, temperature=w.temperature, alpha=w.alpha, beta=w.beta,
+                       accepted_len=acc, next_token=nxt, workspace=ws)
+
+    log(f"warmup {args.warmup} steps over {nrot} rotating input copies")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize(dev)
+
+    stream = torch.cuda.current_stream(dev)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize(dev)
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - wall0
+    ms = ev0.elapsed_time(ev1)
+    ms_per_step = ms / args.steps
+    steps_per_s = 1000.0 / ms_per_step
+    log(f"{ms_per_step * 1000:.2f} us/step (events), wall {wall:.3f} s")
+
+    # the decisions of the timed steps are real: check one against the oracle
+    # later in the tests; here just make sure they are in range
+    a, n = acc.cpu(), nxt.cpu()
+    if bool(((a < 0) | (a > w.gamma)).any()) or bool(((n < 0) | (n >= w.vocab)).any()):
+        log("warning: sentinel outputs in the timed workload")
+
+    alg = algorithmic_bytes(w)
+    achieved = alg / (ms_per_step * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                "kernel": "whole step (row_stats_kernel + select_sample_kernel)" if w.mode == "exact"
+                else "select_sample_kernel", "algorithmic_bytes_per_step": alg}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"timing the CPU oracle for ~{args.cpu_seconds:.0f} s")
+        cpu = cpu_baseline(w, x, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC, "value": round(steps_per_s, 1), "unit": "verify-steps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "mode": w.mode, "batch": w.batch, "gamma": w.gamma, "vocab": w.vocab,
+                   "logits": w.dtype, "temperature": w.temperature, "rotating_copies": nrot},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

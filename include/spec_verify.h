@@ -1,0 +1,176 @@
+/*
+ * spec_verify.h -- C ABI of the fused speculative-sampling verification step
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the verification part of speculative sampling as treated
+ * in "Optimized Speculative Sampling for GPU Hardware Accelerators"
+ * (arXiv 2406.11016):
+ *
+ *   - Sec. 3.1, eq. (1): drafted token x_c (c = 0..gamma-1) is accepted iff
+ *     r_c <= tau_c = min(1, p_c(x_c) / q_c(x_c)); the scan stops at the first
+ *     rejection;
+ *   - Sec. 3.1, eqs. (2)-(3): after a rejection at position L the next token
+ *     is drawn from max(0, p_L - q_L) / sum_x max(0, p_L - q_L);
+ *   - Sec. 3.2.2, eq. (4): in the exact mode p and q are the softmax of the
+ *     target and draft logits;
+ *   - Sec. 3.2.2, eq. (5): in the sigmoid mode they are replaced by
+ *     sigma((z - alpha) / (beta - alpha)), element-wise and unnormalised, with
+ *     the same acceptance test and residual.
+ *
+ * Points the paper leaves open are fixed as follows:
+ *   - when all gamma drafts are accepted the next token is drawn from the
+ *     target row gamma (exact: softmax; sigmoid: p_hat_gamma / sum p_hat_gamma);
+ *   - draws use caller-supplied uniforms: uniforms[b, c] is r_c for c < gamma
+ *     and uniforms[b, gamma] drives the final draw, which is the first index j
+ *     with cumsum(a)[j] > u * sum(a) (inverse CDF over token ids in order);
+ *   - a tie r_c == tau_c accepts; q_c(x_c) == 0 gives tau_c = 1;
+ *   - if the residual mass is zero after a rejection (possible only in the
+ *     sigmoid mode) the next token is drawn from row L of the target instead;
+ *   - the temperature T divides the logits before either mode;
+ *   - token ids are 0-based.
+ *
+ * Layout.  All tensors are dense, row-major, and live in device memory:
+ *   draft_logits   [B, gamma,   V]  dtype
+ *   target_logits  [B, gamma+1, V]  dtype
+ *   draft_tokens   [B, gamma]       int32, the drafted tokens x_c
+ *   uniforms       [B, gamma+1]     fp32 in [0, 1)
+ *   accepted_len   [B]              int32 out, L in [0, gamma]
+ *   next_token     [B]              int32 out, in [0, V)
+ * Rows need no particular alignment; 16-byte aligned rows are read with
+ * 128-bit loads.
+ *
+ * Ownership and concurrency.  Every pointer is owned by the caller.  The
+ * library never allocates, frees, synchronises or prints.  Inputs are only
+ * read; outputs and the workspace are overwritten.  A call enqueues its
+ * kernels on `stream` and returns without waiting: SV_OK means "launched".
+ * The workspace must be zero-filled once before its first use (for example
+ * with spec_verify_workspace_init); the kernels leave it ready for the next
+ * call.  Calls that share a workspace must be ordered (same stream, or
+ * synchronised); concurrent calls need separate workspaces.  There is no
+ * mutable global state: the functions are reentrant and thread-safe.
+ *
+ * Errors.  Invalid arguments are detected on the host before anything is
+ * launched and return a negative status.  Bad data found on the device --
+ * a drafted token outside [0, V), a read row whose distribution is not
+ * finite (a NaN logit; in the exact mode also a +inf logit or a row that is
+ * entirely -inf), or a non-finite or zero final mass -- writes the sentinel
+ * accepted_len[b] = next_token[b] = -1 for that batch element only.  In the
+ * exact mode the rows read are the target and draft rows 0..L and, when
+ * L == gamma, target row gamma; in the sigmoid mode they are the logits at
+ * the drafted tokens of rows 0..L and the full row(s) the next token is drawn
+ * from.  Logits must satisfy |z| / T < 2.3e38 (so that z * log2(e) / T is
+ * finite).
+ */
+#ifndef SPEC_VERIFY_H
+#define SPEC_VERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Storage type of the logits. */
+typedef enum sv_dtype {
+    SV_F32 = 0,   /* IEEE binary32 */
+    SV_F16 = 1,   /* IEEE binary16 */
+    SV_BF16 = 2   /* bfloat16 (upper half of a binary32) */
+} sv_dtype_t;
+
+typedef enum sv_status {
+    SV_OK = 0,
+    SV_ERR_NULL = -1,       /* a required pointer is NULL */
+    SV_ERR_SHAPE = -2,      /* B < 1, gamma < 1 or > SV_MAX_GAMMA, V < 1, or sizes overflow */
+    SV_ERR_DTYPE = -3,      /* unknown sv_dtype_t */
+    SV_ERR_PARAM = -4,      /* temperature not finite and > 0; alpha/beta not finite with alpha < beta */
+    SV_ERR_WORKSPACE = -5,  /* workspace smaller than spec_verify_workspace_bytes() or not 16-byte aligned */
+    SV_ERR_HIP = -6         /* a HIP launch failed (hipGetLastError after the launches) */
+} sv_status_t;
+
+/* Largest number of drafted tokens per step supported by one call. */
+#define SV_MAX_GAMMA 128
+
+/*
+ * Bytes of device workspace a call with these sizes needs (the same value
+ * serves both modes).  Returns 0 for invalid sizes.  The workspace holds the
+ * per-chunk row normalisers (exact mode), per-chunk masses of the final
+ * distribution and one completion counter per batch element.
+ */
+size_t spec_verify_workspace_bytes(int32_t batch, int32_t gamma, int32_t vocab, sv_dtype_t dtype);
+
+/*
+ * Zero-fills `workspace_bytes` bytes of `workspace` on `stream` with a fill
+ * kernel (no memset node, so the call may be captured in a graph).
+ */
+sv_status_t spec_verify_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Exact mode (Sec. 3.1 with the softmax of eq. (4)): softmax of every target
+ * and draft row at temperature T, the acceptance test of eq. (1) at the
+ * drafted tokens, the first-rejection scan, and the inverse-CDF draw from the
+ * residual of eqs. (2)-(3) (or from target row gamma when all drafts are
+ * accepted).  The result equals the plain definition up to floating-point
+ * rounding (fp32 element arithmetic, fp64 reductions).
+ */
+sv_status_t spec_verify_exact(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                              const int32_t* draft_tokens, const float* uniforms,
+                              int32_t batch, int32_t gamma, int32_t vocab, float temperature,
+                              int32_t* accepted_len, int32_t* next_token,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Sigmoid mode (Sec. 3.2.2, eq. (5)): p_hat = sigma((z_p / T - alpha) / (beta - alpha))
+ * and q_hat likewise replace the softmax; tau_hat = min(1, p_hat / q_hat) at
+ * the drafted tokens; after a rejection at L the next token is drawn from
+ * max(0, p_hat_L - q_hat_L) normalised.  Only the logits at the drafted
+ * tokens and the row(s) the next token is drawn from are read.  The paper
+ * uses alpha = -beta = -1e3 (speech) and -1e4 (summarisation).
+ */
+sv_status_t spec_verify_sigmoid(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                const int32_t* draft_tokens, const float* uniforms,
+                                int32_t batch, int32_t gamma, int32_t vocab, float temperature,
+                                float alpha, float beta,
+                                int32_t* accepted_len, int32_t* next_token,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Probe variants for testing: the same computation as spec_verify_exact /
+ * spec_verify_sigmoid, additionally writing any of these that is non-NULL
+ * (device pointers):
+ *   tau_out      [B, gamma]      fp64: tau_c of eq. (1) (or its sigmoid form)
+ *                                for every c (NaN where a row is unreadable);
+ *   weight_out   [B, V]          fp32: the unnormalised weights a(x) of the
+ *                                distribution the next token is drawn from;
+ *   mass_out     [B]             fp64: their sum b;
+ *   lognorm_out  [B, 2*gamma+1]  fp64 (exact mode only): log sum_x exp(z_r(x)/T)
+ *                                of target rows 0..gamma, then draft rows
+ *                                0..gamma-1.
+ * Rows with the sentinel leave weight_out and mass_out unspecified.
+ */
+sv_status_t spec_verify_exact_probe(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                    const int32_t* draft_tokens, const float* uniforms,
+                                    int32_t batch, int32_t gamma, int32_t vocab, float temperature,
+                                    int32_t* accepted_len, int32_t* next_token,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                    double* tau_out, float* weight_out, double* mass_out,
+                                    double* lognorm_out);
+
+sv_status_t spec_verify_sigmoid_probe(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                      const int32_t* draft_tokens, const float* uniforms,
+                                      int32_t batch, int32_t gamma, int32_t vocab, float temperature,
+                                      float alpha, float beta,
+                                      int32_t* accepted_len, int32_t* next_token,
+                                      void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                      double* tau_out, float* weight_out, double* mass_out);
+
+/* Static description of a status code. */
+const char* spec_verify_status_string(sv_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPEC_VERIFY_H */

@@ -41,7 +41,10 @@ Readings where the paper is silent (each is also listed in the design notes):
    finite (NaN logit, +inf logit in exact mode, an all ``-inf`` row in exact
    mode), or a non-finite / zero final mass yields the sentinel
    ``accepted_len = next_token = -1`` for that batch element.  Rows after the
-   first rejection are not read.
+   first rejection are not read.  In the exact mode a row is read whole (its
+   softmax needs every logit); the sigmoid mode is element-wise, so for the
+   drafts it examines it reads only the values at the drafted tokens, and it
+   reads whole only the row(s) the next token is drawn from.
 """
 from __future__ import annotations
 
@@ -199,7 +202,10 @@ def verify(draft_logits: np.ndarray, target_logits: np.ndarray,
     with np.errstate(invalid="ignore"):
         tau = acceptance_ratio(p_x, q_x)
     accepted = r[:, :gamma] <= tau
-    row_ok = row_ok_p[:, :gamma] & row_ok_q & np.isfinite(tau)
+    if mode == "exact":
+        row_ok = row_ok_p[:, :gamma] & row_ok_q & np.isfinite(tau)
+    else:
+        row_ok = np.isfinite(tau)
 
     # first rejection; an unreadable row also ends the scan (as a sentinel)
     stop = (~accepted) | (~row_ok)
@@ -220,7 +226,8 @@ def verify(draft_logits: np.ndarray, target_logits: np.ndarray,
     with np.errstate(invalid="ignore"):
         a_res, b_res = max_norm(rows_p - rows_q)
     rejected = L < gamma
-    fallback = rejected & ~(b_res > 0.0)
+    bad |= rejected & ~np.isfinite(b_res)
+    fallback = rejected & (b_res == 0.0)
     use_p = (~rejected) | fallback
     weights = np.where(use_p[:, None], rows_p, a_res)
     mass = np.where(use_p, np.sum(rows_p, axis=-1), b_res)

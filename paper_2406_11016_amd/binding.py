@@ -1,0 +1,203 @@
+"""Python binding of ``libspec_verify.so`` (ctypes; argument marshalling only).
+
+Every step of the verification runs in the library's HIP kernels.  PyTorch is
+used for device memory and streams: tensors are passed as raw device pointers
+together with the current HIP stream.  There is no fallback: if the library
+is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libspec_verify.so")
+
+SV_F32, SV_F16, SV_BF16 = 0, 1, 2
+DTYPE_CODES = {torch.float32: SV_F32, torch.float16: SV_F16, torch.bfloat16: SV_BF16}
+STORAGE_TORCH_DTYPES = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+MAX_GAMMA = 128
+
+SYMBOLS = (
+    "spec_verify_workspace_bytes",
+    "spec_verify_workspace_init",
+    "spec_verify_exact",
+    "spec_verify_sigmoid",
+    "spec_verify_exact_probe",
+    "spec_verify_sigmoid_probe",
+    "spec_verify_status_string",
+)
+
+
+class SpecVerifyError(RuntimeError):
+    pass
+
+
+_lib = None
+
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_f32 = ctypes.c_float
+_sz = ctypes.c_size_t
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise SpecVerifyError(
+            f"{path} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'` "
+            "or `python paper_2406_11016_amd/build.py`")
+    lib = ctypes.CDLL(path)
+    lib.spec_verify_workspace_bytes.argtypes = [_i32, _i32, _i32, ctypes.c_int]
+    lib.spec_verify_workspace_bytes.restype = _sz
+    lib.spec_verify_workspace_init.argtypes = [_vp, _sz, _vp]
+    lib.spec_verify_workspace_init.restype = ctypes.c_int
+    common = [_vp, _vp, ctypes.c_int, _vp, _vp, _i32, _i32, _i32, _f32]
+    outs = [_vp, _vp, _vp, _sz, _vp]
+    lib.spec_verify_exact.argtypes = common + outs
+    lib.spec_verify_exact.restype = ctypes.c_int
+    lib.spec_verify_sigmoid.argtypes = common + [_f32, _f32] + outs
+    lib.spec_verify_sigmoid.restype = ctypes.c_int
+    lib.spec_verify_exact_probe.argtypes = common + outs + [_vp, _vp, _vp, _vp]
+    lib.spec_verify_exact_probe.restype = ctypes.c_int
+    lib.spec_verify_sigmoid_probe.argtypes = common + [_f32, _f32] + outs + [_vp, _vp, _vp]
+    lib.spec_verify_sigmoid_probe.restype = ctypes.c_int
+    lib.spec_verify_status_string.argtypes = [ctypes.c_int]
+    lib.spec_verify_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().spec_verify_status_string(status).decode()
+
+
+def _check(status: int, what: str) -> None:
+    if status != 0:
+        raise SpecVerifyError(f"{what}: {status_string(status)} (status {status})")
+
+
+def workspace_bytes(batch: int, gamma: int, vocab: int, dtype) -> int:
+    code = DTYPE_CODES[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    n = load_library().spec_verify_workspace_bytes(batch, gamma, vocab, code)
+    if n == 0:
+        raise SpecVerifyError(f"invalid sizes: batch={batch} gamma={gamma} vocab={vocab}")
+    return int(n)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def new_workspace(batch: int, gamma: int, vocab: int, dtype, device) -> torch.Tensor:
+    """A zero-filled workspace (reusable across ordered calls of these sizes)."""
+    n = workspace_bytes(batch, gamma, vocab, dtype)
+    return torch.zeros((n + 15) // 16 * 16, dtype=torch.uint8, device=device)
+
+
+def init_workspace(ws: torch.Tensor) -> None:
+    lib = load_library()
+    _check(lib.spec_verify_workspace_init(_ptr(ws), ws.numel() // 16 * 16, _stream(ws.device)),
+           "spec_verify_workspace_init")
+
+
+@dataclass
+class Probe:
+    tau: torch.Tensor          # [B, gamma] fp64
+    weights: torch.Tensor      # [B, V] fp32 (unnormalised a(x))
+    mass: torch.Tensor         # [B] fp64
+    lognorm: Optional[torch.Tensor] = None  # [B, 2 gamma + 1] fp64 (exact mode)
+
+
+def _validate(draft, target, tokens, uniforms):
+    for name, t in (("draft", draft), ("target", target), ("tokens", tokens), ("uniforms", uniforms)):
+        if not t.is_cuda:
+            raise SpecVerifyError(f"{name} must be a device tensor")
+        if not t.is_contiguous():
+            raise SpecVerifyError(f"{name} must be contiguous")
+    if draft.dtype not in DTYPE_CODES or target.dtype != draft.dtype:
+        raise SpecVerifyError(f"logits must share one of {list(DTYPE_CODES)}; got {draft.dtype}/{target.dtype}")
+    if draft.dim() != 3 or target.dim() != 3:
+        raise SpecVerifyError("logits must be [B, gamma, V] and [B, gamma+1, V]")
+    B, g, V = draft.shape
+    if tuple(target.shape) != (B, g + 1, V):
+        raise SpecVerifyError(f"target shape {tuple(target.shape)} != {(B, g + 1, V)}")
+    if tokens.dtype != torch.int32 or tuple(tokens.shape) != (B, g):
+        raise SpecVerifyError("tokens must be int32 [B, gamma]")
+    if uniforms.dtype != torch.float32 or tuple(uniforms.shape) != (B, g + 1):
+        raise SpecVerifyError("uniforms must be float32 [B, gamma+1]")
+    return B, g, V
+
+
+def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, uniforms: torch.Tensor, *,
+           mode: str = "exact", temperature: float = 1.0, alpha: float = -1.0e4, beta: float = 1.0e4,
+           accepted_len: Optional[torch.Tensor] = None, next_token: Optional[torch.Tensor] = None,
+           workspace: Optional[torch.Tensor] = None, probe: bool = False):
+    """One verification step on the current stream.
+
+    Returns ``(accepted_len, next_token)`` (int32 [B] device tensors), plus a
+    :class:`Probe` when ``probe`` is true.  ``workspace`` (zero-filled before
+    its first use) may be passed to avoid an allocation per call.
+    """
+    if mode not in ("exact", "sigmoid"):
+        raise ValueError(mode)
+    lib = load_library()
+    B, g, V = _validate(draft, target, tokens, uniforms)
+    dev = draft.device
+    if accepted_len is None:
+        accepted_len = torch.empty(B, dtype=torch.int32, device=dev)
+    if next_token is None:
+        next_token = torch.empty(B, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = new_workspace(B, g, V, draft.dtype, dev)
+    code = DTYPE_CODES[draft.dtype]
+    head = [_ptr(draft), _ptr(target), code, _ptr(tokens), _ptr(uniforms), B, g, V, float(temperature)]
+    tail = [_ptr(accepted_len), _ptr(next_token), _ptr(workspace), workspace.numel(), _stream(dev)]
+    pr = None
+    if probe:
+        pr = Probe(tau=torch.full((B, g), float("nan"), dtype=torch.float64, device=dev),
+                   weights=torch.zeros((B, V), dtype=torch.float32, device=dev),
+                   mass=torch.full((B,), float("nan"), dtype=torch.float64, device=dev),
+                   lognorm=(torch.full((B, 2 * g + 1), float("nan"), dtype=torch.float64, device=dev)
+                            if mode == "exact" else None))
+    if mode == "exact":
+        if probe:
+            st = lib.spec_verify_exact_probe(*head, *tail, _ptr(pr.tau), _ptr(pr.weights), _ptr(pr.mass),
+                                             _ptr(pr.lognorm))
+        else:
+            st = lib.spec_verify_exact(*head, *tail)
+    else:
+        ab = [float(alpha), float(beta)]
+        if probe:
+            st = lib.spec_verify_sigmoid_probe(*head, *ab, *tail, _ptr(pr.tau), _ptr(pr.weights), _ptr(pr.mass))
+        else:
+            st = lib.spec_verify_sigmoid(*head, *ab, *tail)
+    _check(st, f"spec_verify_{mode}")
+    return (accepted_len, next_token, pr) if probe else (accepted_len, next_token)
+
+
+def to_device(inputs, device="cuda"):
+    """Upload generator output (host NumPy arrays in storage form) to device tensors."""
+    import numpy as np
+    tdt = STORAGE_TORCH_DTYPES[inputs.dtype]
+    if inputs.dtype == "bf16":
+        d = torch.from_numpy(np.ascontiguousarray(inputs.draft).view(np.int16)).view(torch.bfloat16)
+        t = torch.from_numpy(np.ascontiguousarray(inputs.target).view(np.int16)).view(torch.bfloat16)
+    else:
+        d = torch.from_numpy(np.ascontiguousarray(inputs.draft))
+        t = torch.from_numpy(np.ascontiguousarray(inputs.target))
+    assert d.dtype == tdt
+    return (d.to(device), t.to(device),
+            torch.from_numpy(np.ascontiguousarray(inputs.tokens)).to(device),
+            torch.from_numpy(np.ascontiguousarray(inputs.uniforms)).to(device))

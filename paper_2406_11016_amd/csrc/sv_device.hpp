@@ -1,0 +1,224 @@
+// Device primitives of the verification kernels (gfx950, wave64).
+//
+// Storage-type traits and 128-bit row loaders, the one-pass row normaliser
+// (running power-of-two reference plus fp64 sum), and deterministic wave64 /
+// workgroup reductions and scans.  Every reduction here has a fixed
+// combination order, so a row's result depends only on its values and the
+// chunk geometry -- never on the row's address, the launch order or timing.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+namespace sv {
+
+constexpr int kThreads = 256;            // threads per workgroup (4 wave64s)
+constexpr int kWave = 64;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kMaxGamma = 128;
+constexpr int kMaxRows = 2 * kMaxGamma + 1;
+constexpr int kUnroll = 8;               // 16-byte loads in flight per thread
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// One chunk's contribution to a row normaliser: sum_x 2^(w(x) log2e - k) = s.
+struct RowPartial {
+    double s;
+    float k;
+    float pad;
+};
+
+// ---------------------------------------------------------------------------
+// storage types: E elements per 16-byte vector
+// ---------------------------------------------------------------------------
+struct F32 {
+    using T = float;
+    static constexpr int E = 4;
+};
+struct F16 {
+    using T = _Float16;
+    static constexpr int E = 8;
+};
+struct BF16 {
+    using T = uint16_t;  // raw bfloat16 bits
+    static constexpr int E = 8;
+};
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(_Float16 v) { return (float)v; }
+__device__ __forceinline__ float to_f32(uint16_t v) { return __uint_as_float((uint32_t)v << 16); }
+
+template <class D>
+__device__ __forceinline__ void unpack(const u32x4 r, float (&x)[D::E]);
+
+template <>
+__device__ __forceinline__ void unpack<F32>(const u32x4 r, float (&x)[4]) {
+    x[0] = __uint_as_float(r.x);
+    x[1] = __uint_as_float(r.y);
+    x[2] = __uint_as_float(r.z);
+    x[3] = __uint_as_float(r.w);
+}
+
+template <>
+__device__ __forceinline__ void unpack<BF16>(const u32x4 r, float (&x)[8]) {
+    // bf16 is the upper half of a binary32: shift the low half up, mask the high half.
+    x[0] = __uint_as_float(r.x << 16);
+    x[1] = __uint_as_float(r.x & 0xffff0000u);
+    x[2] = __uint_as_float(r.y << 16);
+    x[3] = __uint_as_float(r.y & 0xffff0000u);
+    x[4] = __uint_as_float(r.z << 16);
+    x[5] = __uint_as_float(r.z & 0xffff0000u);
+    x[6] = __uint_as_float(r.w << 16);
+    x[7] = __uint_as_float(r.w & 0xffff0000u);
+}
+
+template <>
+__device__ __forceinline__ void unpack<F16>(const u32x4 r, float (&x)[8]) {
+    const f16x8 h = __builtin_bit_cast(f16x8, r);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = (float)h[e];
+}
+
+template <class D>
+__device__ __forceinline__ u32x4 load16(const typename D::T* p) {
+    return *reinterpret_cast<const u32x4*>(p);
+}
+
+// Elements i..i+E-1 of a row with element-wise loads (any alignment); indices
+// at or beyond `end` read as `pad`.
+template <class D>
+__device__ __forceinline__ void load_elems(const typename D::T* row, int i, int end, float pad,
+                                           float (&x)[D::E]) {
+#pragma unroll
+    for (int e = 0; e < D::E; ++e) x[e] = (i + e < end) ? to_f32(row[i + e]) : pad;
+}
+
+// ---------------------------------------------------------------------------
+// wave64 / workgroup reductions (butterfly: every lane ends with the same bits)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+__device__ __forceinline__ int wave_max_int(int v) {
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+// Sum over the workgroup in a fixed order; the result is valid in every thread.
+__device__ __forceinline__ double block_sum(double v, double* scratch /* [kWaves] in LDS */) {
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    v = wave_sum(v);
+    __syncthreads();
+    if (lane == 0) scratch[wave] = v;
+    __syncthreads();
+    double s = scratch[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) s += scratch[w];
+    return s;
+}
+
+// Inclusive scan over the workgroup in thread order (fixed order, fp64).
+// Returns the inclusive prefix; `*total` receives the workgroup total.
+__device__ __forceinline__ double block_inclusive_scan(double v, double* scratch /* [kWaves] */,
+                                                       double* total) {
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const double n = __shfl_up(v, o, kWave);
+        if (lane >= o) v += n;
+    }
+    __syncthreads();
+    if (lane == kWave - 1) scratch[wave] = v;
+    __syncthreads();
+    double off = 0.0;
+    for (int w = 0; w < wave; ++w) off += scratch[w];
+    double t = 0.0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) t += scratch[w];
+    *total = t;
+    return off + v;
+}
+
+// ---------------------------------------------------------------------------
+// row normaliser: log sum_x exp(w(x)) = ln2 * (k + log2 s)
+//
+// With y = z * c (c = log2(e) / T) the running reference k is an integer
+// (a ceiling of the running maximum of y), so rescaling the running sum when
+// the maximum grows is an exact power-of-two scaling.  Each term
+// 2^(fma(z, c, -k)) is evaluated from one correctly rounded argument, and the
+// sum is kept in fp64.
+// ---------------------------------------------------------------------------
+struct Lse {
+    float k;   // integral reference, or -inf while nothing finite was seen
+    double s;  // sum of 2^(y - k)
+};
+
+// Exponent difference for ldexp: -inf and NaN map to a large negative value.
+__device__ __forceinline__ int exp_delta(float d) { return (int)fmaxf(d, -2048.0f); }
+
+__device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
+    const float k = fmaxf(a.k, b.k);
+    return Lse{k, ldexp(a.s, exp_delta(a.k - k)) + ldexp(b.s, exp_delta(b.k - k))};
+}
+
+template <int E>
+__device__ __forceinline__ void lse_absorb(Lse& st, const float (&x)[E], float c) {
+    float m = x[0];
+#pragma unroll
+    for (int e = 1; e < E; ++e) m = fmaxf(m, x[e]);
+    const float kv = ceilf(m * c);
+    if (kv > st.k) {
+        st.s = ldexp(st.s, exp_delta(st.k - kv));
+        st.k = kv;
+    }
+    const float nk = (st.k == -INFINITY) ? 0.0f : -st.k;
+    float t[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) t[e] = __builtin_amdgcn_exp2f(fmaf(x[e], c, nk));
+#pragma unroll
+    for (int w = E / 2; w >= 1; w /= 2) {
+#pragma unroll
+        for (int e = 0; e < w; ++e) t[e] += t[e + w];
+    }
+    st.s += (double)t[0];
+}
+
+__device__ __forceinline__ Lse wave_lse(Lse st) {
+    const float kw = wave_max(st.k);
+    return Lse{kw, wave_sum(ldexp(st.s, exp_delta(st.k - kw)))};
+}
+
+// Valid in thread 0 only.
+__device__ __forceinline__ Lse block_lse(Lse st, float* sk /* [kWaves] */, double* ss /* [kWaves] */) {
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    const Lse w = wave_lse(st);
+    if (lane == 0) {
+        sk[wave] = w.k;
+        ss[wave] = w.s;
+    }
+    __syncthreads();
+    Lse out{-INFINITY, 0.0};
+    if (threadIdx.x == 0) {
+        out = Lse{sk[0], ss[0]};
+#pragma unroll
+        for (int i = 1; i < kWaves; ++i) out = lse_merge(out, Lse{sk[i], ss[i]});
+    }
+    return out;
+}
+
+}  // namespace sv

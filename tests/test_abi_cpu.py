@@ -1,0 +1,123 @@
+"""The C ABI on the host: the library loads, exports every function the header
+declares, sizes its workspace, and rejects invalid arguments before launching
+anything (none of these calls reaches the GPU)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2406_11016_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "spec_verify.h")
+
+SV_OK, SV_ERR_NULL, SV_ERR_SHAPE, SV_ERR_DTYPE, SV_ERR_PARAM, SV_ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(spec_verify_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        pytest.fail("libspec_verify.so not built; run __graft_entry__.build()")
+    return binding.load_library()
+
+
+def test_header_declares_the_boundary():
+    fns = declared_functions()
+    assert fns == sorted(binding.SYMBOLS), fns
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", binding.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (spec_verify_\w+)", out))
+    for fn in declared_functions():
+        assert fn in exported, fn
+        assert getattr(lib, fn) is not None
+
+
+def test_status_strings(lib):
+    for st in (0, -1, -2, -3, -4, -5, -6):
+        assert binding.status_string(st)
+    assert binding.status_string(0) == "ok"
+    assert "unknown" in binding.status_string(7)
+
+
+def test_workspace_bytes(lib):
+    f = lib.spec_verify_workspace_bytes
+    for args in [(1, 5, 51865, 0), (64, 8, 128256, 2), (32, 10, 50272, 1), (1, 1, 1, 0), (3, 128, 7, 1)]:
+        n = f(*args)
+        assert n > 0 and n % 256 == 0
+    assert f(64, 8, 128256, 2) >= 64 * 17 * 16       # at least one normaliser partial per row
+    for bad in [(0, 5, 100, 0), (1, 0, 100, 0), (1, 129, 100, 0), (1, 5, 0, 0), (1, 5, 100, 3), (-1, 5, 100, 0)]:
+        assert f(*bad) == 0
+
+
+def _args(**kw):
+    base = dict(draft=0x1000, target=0x2000, dtype=0, tokens=0x3000, uniforms=0x4000, B=2, gamma=3, V=100,
+                T=1.0, acc=0x5000, nxt=0x6000, ws=0x7000, ws_bytes=1 << 20, stream=None)
+    base.update(kw)
+    return base
+
+
+def _exact(lib, a):
+    return lib.spec_verify_exact(a["draft"], a["target"], a["dtype"], a["tokens"], a["uniforms"], a["B"],
+                                 a["gamma"], a["V"], a["T"], a["acc"], a["nxt"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+def _sigmoid(lib, a, alpha=-1e4, beta=1e4):
+    return lib.spec_verify_sigmoid(a["draft"], a["target"], a["dtype"], a["tokens"], a["uniforms"], a["B"],
+                                   a["gamma"], a["V"], a["T"], alpha, beta, a["acc"], a["nxt"], a["ws"],
+                                   a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("field", ["draft", "target", "tokens", "uniforms", "acc", "nxt", "ws"])
+def test_null_pointers_rejected(lib, field):
+    assert _exact(lib, _args(**{field: None})) == SV_ERR_NULL
+    assert _sigmoid(lib, _args(**{field: None})) == SV_ERR_NULL
+
+
+def test_invalid_shapes_dtype_params_workspace(lib):
+    assert _exact(lib, _args(B=0)) == SV_ERR_SHAPE
+    assert _exact(lib, _args(gamma=0)) == SV_ERR_SHAPE
+    assert _exact(lib, _args(gamma=129)) == SV_ERR_SHAPE
+    assert _exact(lib, _args(V=0)) == SV_ERR_SHAPE
+    assert _exact(lib, _args(dtype=5)) == SV_ERR_DTYPE
+    for T in (0.0, -1.0, float("inf"), float("nan"), 1e-45):
+        assert _exact(lib, _args(T=T)) == SV_ERR_PARAM, T
+    for alpha, beta in [(1.0, 1.0), (2.0, -2.0), (float("nan"), 1.0), (-1.0, float("inf"))]:
+        assert _sigmoid(lib, _args(), alpha, beta) == SV_ERR_PARAM
+    need = lib.spec_verify_workspace_bytes(2, 3, 100, 0)
+    assert _exact(lib, _args(ws_bytes=need - 1)) == SV_ERR_WORKSPACE
+    assert _exact(lib, _args(ws=0x7004)) == SV_ERR_WORKSPACE
+    assert lib.spec_verify_workspace_init(None, 256, None) == SV_ERR_NULL
+    assert lib.spec_verify_workspace_init(0x7004, 256, None) == SV_ERR_WORKSPACE
+
+
+def test_probe_entry_points_validate_too(lib):
+    a = _args(B=0)
+    st = lib.spec_verify_exact_probe(a["draft"], a["target"], a["dtype"], a["tokens"], a["uniforms"], a["B"],
+                                     a["gamma"], a["V"], a["T"], a["acc"], a["nxt"], a["ws"], a["ws_bytes"],
+                                     a["stream"], None, None, None, None)
+    assert st == SV_ERR_SHAPE
+    a = _args(T=-1.0)
+    st = lib.spec_verify_sigmoid_probe(a["draft"], a["target"], a["dtype"], a["tokens"], a["uniforms"], a["B"],
+                                       a["gamma"], a["V"], a["T"], -10.0, 10.0, a["acc"], a["nxt"], a["ws"],
+                                       a["ws_bytes"], a["stream"], None, None, None)
+    assert st == SV_ERR_PARAM
+
+
+def test_no_cpu_fallback_in_binding():
+    src = open(os.path.join(ROOT, "paper_2406_11016_amd", "binding.py")).read()
+    assert "oracle" not in src
+    for f in os.listdir(os.path.join(ROOT, "paper_2406_11016_amd")):
+        if f.endswith(".py"):
+            assert "import oracle" not in open(os.path.join(ROOT, "paper_2406_11016_amd", f)).read()
+            assert "from oracle" not in open(os.path.join(ROOT, "paper_2406_11016_amd", f)).read()

@@ -1,0 +1,222 @@
+"""Parity of the HIP path with the CPU oracle, through the C ABI.
+
+Decisions (accepted_len, next_token) must match bit for bit except where the
+oracle places a uniform within 1e-6 of its threshold (counted and reported);
+probabilities must match within 1e-5 relative (fp32 logits) or 2e-3
+(fp16 / bf16 logits)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2406_11016_amd import binding
+from paper_2406_11016_amd import workloads as W
+from tests.golden_util import example_arrays
+from tests.gpu_util import compare, run_gpu, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    binding.load_library()
+    torch.cuda.init()
+
+
+def _report(label, x, nflag):
+    print(f"[parity] {label}: B={x.batch} gamma={x.gamma} V={x.vocab} {x.dtype} {x.mode} flagged={nflag}",
+          flush=True)
+
+
+# --- reduced versions of every named workload: several tiles, ragged tails --
+
+SMALL = [
+    ("exact_b1_g5_v51865_f32", dict(vocab=9001)),
+    ("exact_b1_g10_v32000_f16", dict(vocab=6007)),
+    ("exact_b16_g5_v51865_f32", dict(vocab=5003)),
+    ("exact_b64_g8_v128256_bf16", dict(batch=8, vocab=20011)),
+    ("sigmoid_b32_g10_v50272_f16_t0.7", dict(batch=8, vocab=10007)),
+]
+
+
+@pytest.mark.parametrize("name,over", SMALL, ids=[s[0] for s in SMALL])
+def test_small_workloads(name, over):
+    w = W.WORKLOADS[name].with_(**over)
+    x = W.generate(w)
+    nflag = compare(x, run_gpu(x), run_oracle(x), label=name)
+    _report(name + " (reduced)", x, nflag)
+
+
+# --- the named workloads at full size (the shapes the benchmark times) ------
+
+@pytest.mark.parametrize("name", list(W.WORKLOADS))
+def test_full_size_workloads(name):
+    x = W.generate(W.WORKLOADS[name])
+    nflag = compare(x, run_gpu(x), run_oracle(x), label=name)
+    _report(name, x, nflag)
+
+
+# --- edge cases ---------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("V", [1, 2, 7, 8, 63, 64, 65, 4097])
+def test_vocab_edge_sizes(dtype, V):
+    for gamma, B in [(1, 1), (3, 5)]:
+        x = W.small_case(B, gamma, V, dtype, seed=100 + V)
+        compare(x, run_gpu(x), run_oracle(x), label=f"V={V} {dtype} g={gamma}")
+
+
+@pytest.mark.parametrize("mode", ["exact", "sigmoid"])
+def test_unaligned_rows_and_offsets(mode):
+    # odd V in fp32: every row after the first starts off a 16-byte boundary
+    x = W.small_case(7, 4, 12347, "f32", mode=mode, seed=3, alpha=-1e3, beta=1e3)
+    compare(x, run_gpu(x), run_oracle(x), label="odd V f32")
+
+
+@pytest.mark.parametrize("T", [0.7, 1.0, 1.3])
+@pytest.mark.parametrize("mode", ["exact", "sigmoid"])
+def test_temperatures(T, mode):
+    x = W.small_case(6, 5, 3001, "f16", mode=mode, seed=11, temperature=T, alpha=-1e3, beta=1e3)
+    compare(x, run_gpu(x), run_oracle(x), label=f"T={T} {mode}")
+
+
+def test_identical_rows_accept_every_draft_bit_exactly():
+    x = W.small_case(16, 6, 20000, "f32", seed=5)
+    x.draft[:] = x.target[:, :6]
+    x.uniforms[:, :6] = W.UNIFORM_MAX          # the largest uniform still accepts tau = 1
+    for mode in ("exact", "sigmoid"):
+        x.mode = mode
+        g = run_gpu(x)
+        assert np.all(g.accepted_len == 6), (mode, g.accepted_len)
+        assert np.all(g.tau == 1.0), mode
+        compare(x, g, run_oracle(x), label=f"p==q {mode}")
+
+
+def test_token_extremes_and_uniform_extremes():
+    x = W.small_case(8, 4, 777, "bf16", seed=9)
+    x.tokens[0, :] = 0
+    x.tokens[1, :] = 776
+    x.uniforms[2, :] = 0.0
+    x.uniforms[3, :] = W.UNIFORM_MAX
+    x.uniforms[4, -1] = 0.0
+    x.uniforms[5, -1] = W.UNIFORM_MAX
+    compare(x, run_gpu(x), run_oracle(x), label="extremes")
+
+
+@pytest.mark.parametrize("mode", ["exact", "sigmoid"])
+def test_masked_logits(mode):
+    x = W.small_case(12, 4, 3000, "f32", mode=mode, seed=21, alpha=-1e3, beta=1e3)
+    rng = np.random.default_rng(0)
+    mask_t = rng.random(x.target.shape) < 0.5
+    mask_d = rng.random(x.draft.shape) < 0.5
+    x.target[mask_t] = -np.inf
+    x.draft[mask_d] = -np.inf
+    # keep some drafted tokens on target-masked positions (reject) and some on
+    # draft-masked positions (tau = 1)
+    compare(x, run_gpu(x), run_oracle(x), label=f"masked {mode}")
+
+
+def test_fp16_extremes():
+    x = W.small_case(4, 3, 1000, "f16", seed=31)
+    x.target[0, 0, 10] = np.float16(65504.0)
+    x.draft[1, 0, 20] = np.float16(-65504.0)
+    x.target[2, :, :] = np.float16(65504.0)
+    x.draft[3, :, :] = np.float16(-65504.0)
+    compare(x, run_gpu(x), run_oracle(x), label="fp16 extremes")
+
+
+@pytest.mark.parametrize("mode", ["exact", "sigmoid"])
+def test_sentinels(mode):
+    x = W.small_case(6, 3, 500, "f32", mode=mode, seed=41, alpha=-1e3, beta=1e3)
+    x.tokens[0, 1] = 500                      # invalid token
+    x.tokens[1, 0] = -3
+    x.target[2, 0, :] = np.nan                # NaN in a row read by both modes
+    x.uniforms[3, :] = 0.0                    # accept everything -> bonus row read
+    x.target[3, 3, :] = np.nan
+    x.draft[4, 2, 7] = np.nan                 # NaN away from the token: exact reads it, sigmoid does not
+    x.tokens[4, 2] = 8
+    x.uniforms[4, :3] = 0.0
+    if mode == "exact":
+        x.target[5, :2, :] = -np.inf          # all -inf rows (exact: unreadable)
+    g = run_gpu(x)
+    o = run_oracle(x)
+    assert g.accepted_len.tolist() == o.accepted_len.tolist(), (g.accepted_len, o.accepted_len)
+    assert g.next_token.tolist() == o.next_token.tolist(), (g.next_token, o.next_token)
+    assert g.accepted_len[0] == -1 and g.accepted_len[1] == -1 and g.accepted_len[2] == -1
+    assert g.accepted_len[3] == -1
+
+
+@pytest.mark.parametrize("ab", [10.0, 1e3, 1e4, 1e5])
+def test_sigmoid_scaling_constants(ab):
+    x = W.small_case(16, 10, 50272, "f16", mode="sigmoid", seed=51, temperature=0.7, alpha=-ab, beta=ab)
+    g = run_gpu(x)
+    assert np.all(np.isfinite(g.tau))
+    compare(x, g, run_oracle(x), label=f"sigmoid +-{ab:g}")
+
+
+def test_sigmoid_zero_residual_fallback():
+    # p_hat <= q_hat everywhere in row 0 and the draft rejected: draw from p_hat_0
+    x = W.small_case(4, 2, 333, "f32", mode="sigmoid", seed=61, alpha=-10.0, beta=10.0)
+    x.draft[:, 0, :] = x.target[:, 0, :] + 1.0
+    x.uniforms[:, 0] = 0.999999
+    g = run_gpu(x)
+    o = run_oracle(x)
+    assert np.all(o.fallback)
+    compare(x, g, o, label="fallback")
+
+
+@pytest.mark.parametrize("idx", range(8))
+def test_golden_examples_on_gpu(golden_examples, idx):
+    ex = golden_examples[idx]
+    draft, target, tokens, uniforms = example_arrays(ex, dtype=np.float32)
+    x = W.Inputs(draft, target, tokens, uniforms.astype(np.float32), "f32", ex["mode"], ex["temperature"],
+                 ex["alpha"], ex["beta"])
+    g = run_gpu(x)
+    assert int(g.accepted_len[0]) == ex["expect"]["accepted_len"], ex["name"]
+    assert int(g.next_token[0]) == ex["expect"]["next_token"], ex["name"]
+
+
+def test_deterministic_and_workspace_reuse():
+    big = W.small_case(16, 8, 40000, "bf16", seed=71)
+    small = W.small_case(3, 2, 999, "bf16", seed=72)
+    ws = binding.new_workspace(16, 8, 40000, torch.bfloat16, "cuda")
+    first = run_gpu(big, workspace=ws)
+    for _ in range(20):
+        again = run_gpu(big, workspace=ws)
+        assert np.array_equal(first.accepted_len, again.accepted_len)
+        assert np.array_equal(first.next_token, again.next_token)
+        assert np.array_equal(first.tau, again.tau) and np.array_equal(first.weights, again.weights)
+    assert binding.workspace_bytes(3, 2, 999, torch.bfloat16) <= ws.numel()
+    compare(small, run_gpu(small, workspace=ws), run_oracle(small), label="reuse smaller")
+    compare(big, run_gpu(big, workspace=ws), run_oracle(big), label="reuse bigger again")
+
+
+def test_gpu_emits_target_distribution_tiny_vocab():
+    """10^6 seeded steps through the GPU with fixed rows: the token emitted at
+    each position is distributed as p (3-sigma per category)."""
+    gamma, V, n = 3, 8, 1_000_000
+    g = np.random.Generator(np.random.PCG64(808))
+    z_p = g.normal(0, 1.5, size=(gamma + 1, V)).astype(np.float32)
+    z_q = (z_p[:gamma] + g.normal(0, 1.0, size=(gamma, V))).astype(np.float32)
+    tokens = np.stack([W.gumbel_max_tokens(g, np.broadcast_to(z_q[c].astype(np.float64), (n, V)), 1.0)
+                       for c in range(gamma)], axis=1)
+    u = np.minimum(g.random((n, gamma + 1)).astype(np.float32), W.UNIFORM_MAX)
+    x = W.Inputs(np.ascontiguousarray(np.broadcast_to(z_q, (n, gamma, V))),
+                 np.ascontiguousarray(np.broadcast_to(z_p, (n, gamma + 1, V))), tokens, u, "f32", "exact", 1.0,
+                 -1e4, 1e4)
+    acc, nxt = run_gpu(x, probe=False)
+    assert np.all(acc >= 0)
+    P = np.exp(z_p.astype(np.float64) - z_p.max(-1, keepdims=True))
+    P /= P.sum(-1, keepdims=True)
+    for c in range(gamma + 1):
+        reached = acc >= c
+        emitted = np.where(acc[reached] > c, tokens[reached, min(c, gamma - 1)] if c < gamma else -1,
+                           nxt[reached])
+        m = emitted.size
+        counts = np.bincount(emitted, minlength=V)
+        sigma = np.sqrt(m * P[c] * (1 - P[c]))
+        assert np.all(np.abs(counts - m * P[c]) <= 3 * sigma), (c, counts, m * P[c], sigma)
