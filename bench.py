@@ -159,8 +159,8 @@ def main() -> int:
     achieved = alg / (ms_per_step * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
-                "kernel": "whole step (row_stats_kernel + select_sample_kernel)" if w.mode == "exact"
-                else "select_sample_kernel", "algorithmic_bytes_per_step": alg}
+                "kernel": "whole step (row_stats_kernel + mass_kernel + draw_kernel)" if w.mode == "exact"
+                else "whole step (mass_kernel + draw_kernel)", "algorithmic_bytes_per_step": alg}
 
     cpu = None
     if not args.no_cpu_baseline:

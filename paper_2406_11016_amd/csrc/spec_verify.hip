@@ -2,25 +2,23 @@
 //
 // Method: arXiv 2406.11016, Sec. 3.1 (eqs. (1)-(3)) and Sec. 3.2.2 (eqs. (4)-(5)).
 //
-// Exact mode, two launches on the caller's stream:
-//   row_stats_kernel   grid = B * (2*gamma+1) * nchunk1 workgroups.  Each
-//                      streams one chunk of one logit row exactly once with
-//                      128-bit loads and writes that chunk's contribution to
-//                      the row's softmax normaliser (eq. (4)) to the
-//                      workspace.  This kernel moves every logit byte and
-//                      bounds the step.
-//   select_sample_kernel<exact>  grid = B * nchunk2.  Every workgroup of batch
-//                      element b merges b's chunk normalisers in a fixed order,
-//                      evaluates tau_c (eq. (1)) at the drafted tokens and runs
-//                      the first-rejection scan, so all of them agree on L.
-//                      Each then sums the weights a(x) of the final
-//                      distribution (residual of eqs. (2)-(3), or target row
-//                      gamma) over its chunk of the selected row(s).  The last
-//                      workgroup of b to finish (completion counter) draws the
-//                      next token by inverse CDF: fixed-order prefix over the
-//                      chunk masses, then a workgroup scan inside the chunk the
-//                      draw falls in.
-// Sigmoid mode, one launch: select_sample_kernel<sigmoid>; the element-wise
+// Exact mode, three launches on the caller's stream:
+//   row_stats_kernel  grid = B * (2*gamma+1) * nchunk1 workgroups.  Each
+//                     streams one chunk of one logit row exactly once with
+//                     128-bit loads and writes that chunk's contribution to
+//                     the row's softmax normaliser (eq. (4)).  This kernel
+//                     moves every logit byte and bounds the step.
+//   mass_kernel       grid = B * nchunk2.  Every workgroup of batch element b
+//                     merges b's chunk normalisers in a fixed order, evaluates
+//                     tau_c (eq. (1)) at the drafted tokens and runs the
+//                     first-rejection scan, so all of them agree on L without
+//                     communicating; each then sums the weights a(x) of the
+//                     final distribution (residual of eqs. (2)-(3), or target
+//                     row gamma) over its chunk of the selected row(s).
+//   draw_kernel       grid = B.  Fixed-order prefix over b's chunk masses,
+//                     then a workgroup scan inside the chunk the uniform falls
+//                     in: the inverse-CDF draw of the next token.
+// Sigmoid mode: mass_kernel and draw_kernel only; the element-wise
 // approximation of eq. (5) needs no row normaliser, so only the logits at the
 // drafted tokens and the row(s) the next token is drawn from are read.
 #include <math.h>
@@ -36,7 +34,7 @@ namespace sv {
 
 enum : int { kResidual = 0, kTargetRow = 1 };
 
-constexpr int kMaxScanRounds = 8;        // vectors per thread in the in-chunk scan
+constexpr int kScanVec = 4;              // contiguous vectors per thread in the in-chunk scan
 constexpr int kWantStatsTiles = 2048;    // enough workgroups to fill 256 CUs several times
 constexpr int kWantSampleTiles = 1024;
 constexpr int kStatsTileBytes = 65536;   // at most 64 KiB of one row per stats workgroup
@@ -46,11 +44,6 @@ constexpr int kSampleTileBytes = 32768;
 // weights of the distribution the next token is drawn from
 // ---------------------------------------------------------------------------
 
-// Exact mode, in log2 units: log2 p(x) = z_p(x) c - Lambda_p with c = log2(e)/T
-// and Lambda = k + log2(s) from the row normaliser.  The residual
-// a(x) = max(0, p - q) (eqs. (2)-(3)) is formed as q (2^d - 1) with
-// d = log2 p(x) - log2 q(x), so p == q cancels exactly and small differences
-// keep their relative precision.
 // zp - zq as an unevaluated sum hi + lo (Knuth's two-sum): the difference of two
 // logits is not exact in fp32 when their exponents are far apart (e.g. fp16
 // logits near +-65504 against logits near 1).
@@ -61,6 +54,30 @@ __device__ __forceinline__ void two_diff(float a, float b, float& hi, float& lo)
     if (!__builtin_isfinite(hi)) lo = 0.0f;  // +-inf or NaN differences carry no low part
 }
 
+constexpr float kLn2 = 0.693147180559945309f;
+constexpr float kLog2e = 1.44269504088896341f;
+
+// 2^x with the hardware exponential (about 1 ulp; results below 2^-126 flush to 0).
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// e^x - 1 for 0 <= x <= 0.35 by its Taylor series to degree 7 (truncation
+// below 2e-8 relative), keeping full relative precision for small x.
+__device__ __forceinline__ float expm1_small(float x) {
+    float p = 1.0f / 5040.0f;
+    p = fmaf(p, x, 1.0f / 720.0f);
+    p = fmaf(p, x, 1.0f / 120.0f);
+    p = fmaf(p, x, 1.0f / 24.0f);
+    p = fmaf(p, x, 1.0f / 6.0f);
+    p = fmaf(p, x, 0.5f);
+    p = fmaf(p, x, 1.0f);
+    return p * x;
+}
+
+// Exact mode, in log2 units: log2 p(x) = z_p(x) c - Lambda_p with c = log2(e)/T
+// and Lambda = k + log2(s) from the row normaliser.  The residual
+// a(x) = max(0, p - q) (eqs. (2)-(3)) is formed as q (2^d - 1) with
+// d = log2 p(x) - log2 q(x), so p == q cancels exactly and small differences
+// keep their relative precision.
 struct ExactWeights {
     int kind;
     float c;
@@ -68,19 +85,21 @@ struct ExactWeights {
     float kq, lq_hi, lq_lo;  // draft row
     float d_hi, d_lo;        // Lambda_p - Lambda_q as hi + lo
     __device__ __forceinline__ float operator()(float zp, float zq) const {
-        const float lp = (fmaf(zp, c, -kp) - lp_hi) - lp_lo;
-        if (kind == kTargetRow) return exp2f(lp);
+        if (kind == kTargetRow) return exp2_hw((fmaf(zp, c, -kp) - lp_hi) - lp_lo);
         float dz, dz_lo;
         two_diff(zp, zq, dz, dz_lo);
         const float d = fmaf(dz_lo, c, fmaf(dz, c, -d_hi)) - d_lo;
         if (!(d > 0.0f)) return 0.0f;
-        const float lq = (fmaf(zq, c, -kq) - lq_hi) - lq_lo;
-        if (d <= 0.5f) return exp2f(lq) * expm1f(d * 0.693147180559945309f);
-        return exp2f(lp) - exp2f(lq);
+        const float q = exp2_hw((fmaf(zq, c, -kq) - lq_hi) - lq_lo);
+        if (d <= 0.5f) return q * expm1_small(d * kLn2);
+        return exp2_hw((fmaf(zp, c, -kp) - lp_hi) - lp_lo) - q;
     }
 };
 
-__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + expf(-x)); }
+// sigma(x) = 1 / (1 + e^-x) with the hardware exponential and reciprocal.
+__device__ __forceinline__ float sigm(float x) {
+    return __builtin_amdgcn_rcpf(1.0f + exp2_hw(-x * kLog2e));
+}
 
 // Sigmoid mode, eq. (5): p_hat = sigma(u_p) with u = (z/T - alpha)/(beta - alpha).
 // max(0, p_hat - q_hat) is formed as q_hat (1 - p_hat) expm1(u_p - u_q), exact
@@ -97,28 +116,11 @@ struct SigmoidWeights {
         const float d = fmaf(dz, s, dz_lo * s);
         if (!(d > 0.0f)) return 0.0f;
         const float uq = fmaf(zq, s, s0);
-        if (d <= 20.0f) return sigm(uq) * sigm(-up) * expm1f(d);
+        if (d <= 0.35f) return sigm(uq) * sigm(-up) * expm1_small(d);
+        if (d <= 20.0f) return sigm(uq) * sigm(-up) * (exp2_hw(d * kLog2e) - 1.0f);
         return (up < 0.0f) ? sigm(up) - sigm(uq) : sigm(-uq) - sigm(-up);
     }
 };
-
-// Elements i..i+E-1 (relative to the chunk start) of the selected row pair.
-template <class D>
-__device__ __forceinline__ void load_pair(const typename D::T* rp, const typename D::T* rq, bool two_rows,
-                                          bool fast, int i, int n, float (&zp)[D::E], float (&zq)[D::E]) {
-    constexpr int E = D::E;
-    if (fast && i + E <= n) {
-        unpack<D>(load16<D>(rp + i), zp);
-        if (two_rows) unpack<D>(load16<D>(rq + i), zq);
-    } else {
-        load_elems<D>(rp, i, n, -INFINITY, zp);
-        if (two_rows) load_elems<D>(rq, i, n, -INFINITY, zq);
-    }
-    if (!two_rows) {
-#pragma unroll
-        for (int e = 0; e < E; ++e) zq[e] = -INFINITY;
-    }
-}
 
 template <class D>
 __device__ __forceinline__ bool pair_aligned(const typename D::T* rp, const typename D::T* rq, bool two_rows) {
@@ -126,16 +128,54 @@ __device__ __forceinline__ bool pair_aligned(const typename D::T* rp, const type
     return (a & 15u) == 0;
 }
 
-// Weights of vector v of a chunk (elements beyond n weigh 0).
-template <class D, class W>
-__device__ __forceinline__ void vector_weights(const typename D::T* rp, const typename D::T* rq, bool two_rows,
-                                               bool fast, int v, int n, const W& w, float (&a)[D::E]) {
+// Vectors v0 + u * vstride (u < U) from a chunk of n elements of the selected
+// row pair (rp/rq point at the chunk start).  All 16-byte loads are issued
+// before any is used; elements at or beyond n read as -inf (weight 0), and
+// with one row the draft side is -inf.
+template <class D, int U>
+__device__ __forceinline__ void load_pair_u(const typename D::T* rp, const typename D::T* rq, bool two_rows,
+                                            bool fast, int v0, int vstride, int n, float (&zp)[U][D::E],
+                                            float (&zq)[U][D::E]) {
     constexpr int E = D::E;
-    float zp[E], zq[E];
-    load_pair<D>(rp, rq, two_rows, fast, v * E, n, zp, zq);
+    const int nfull = n / E;
+    if (fast) {
+        u32x4 a[U], c[U];
 #pragma unroll
-    for (int e = 0; e < E; ++e) a[e] = w(zp[e], zq[e]);
+        for (int u = 0; u < U; ++u) {
+            const int v = v0 + u * vstride;
+            if (v < nfull) {
+                a[u] = load16<D>(rp + v * E);
+                if (two_rows) c[u] = load16<D>(rq + v * E);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int v = v0 + u * vstride;
+            if (v < nfull) {
+                unpack<D>(a[u], zp[u]);
+                if (two_rows) unpack<D>(c[u], zq[u]);
+            } else {
+                load_elems<D>(rp, v * E, n, -INFINITY, zp[u]);
+                if (two_rows) load_elems<D>(rq, v * E, n, -INFINITY, zq[u]);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int v = v0 + u * vstride;
+            load_elems<D>(rp, v * E, n, -INFINITY, zp[u]);
+            if (two_rows) load_elems<D>(rq, v * E, n, -INFINITY, zq[u]);
+        }
+    }
+    if (!two_rows) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e) zq[u][e] = -INFINITY;
+    }
 }
+
+constexpr int kPassUnroll = 4;  // vectors per thread per round in the weight pass
 
 // Sum of the weights over one chunk (rp/rq point at the chunk start, n
 // elements); optionally stores every weight.  Valid in every thread.
@@ -146,13 +186,19 @@ __device__ double chunk_weight_sum(const typename D::T* rp, const typename D::T*
     const int nvec = (n + E - 1) / E;
     const bool fast = pair_aligned<D>(rp, rq, two_rows);
     double acc = 0.0;
-    for (int v = threadIdx.x; v < nvec; v += kThreads) {
-        float a[E];
-        vector_weights<D>(rp, rq, two_rows, fast, v, n, w, a);
+    for (int v0 = 0; v0 < nvec; v0 += kPassUnroll * kThreads) {
+        float zp[kPassUnroll][E], zq[kPassUnroll][E];
+        load_pair_u<D, kPassUnroll>(rp, rq, two_rows, fast, v0 + (int)threadIdx.x, kThreads, n, zp, zq);
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-            if (wout != nullptr && v * E + e < n) wout[v * E + e] = a[e];
-            acc += (double)a[e];
+        for (int u = 0; u < kPassUnroll; ++u) {
+            const int v = v0 + u * kThreads + (int)threadIdx.x;
+            if (v >= nvec) continue;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const float a = w(zp[u][e], zq[u][e]);
+                if (wout != nullptr && v * E + e < n) wout[v * E + e] = a;
+                acc += (double)a;
+            }
         }
     }
     return block_sum(acc, scratch);
@@ -174,76 +220,66 @@ __device__ __forceinline__ int block_first(bool pred, int* iscratch /* [kWaves] 
 
 // Index (relative to the chunk start) of the first element whose running
 // weight sum exceeds t, or of the last positive weight if rounding leaves the
-// chunk total at or below t.  Valid in every thread.  Thread i holds vectors
-// i, i + kThreads, ...; the scan runs over rounds of kThreads vectors so that
-// the prefix follows element order.
+// chunk total at or below t.  Valid in every thread.  Thread i owns the
+// contiguous vectors [i * kScanVec, (i + 1) * kScanVec), so one workgroup scan
+// of the per-thread sums follows element order.  Needs n <= kScanVec * kThreads * E.
 template <class D, class W>
 __device__ int chunk_find(const typename D::T* rp, const typename D::T* rq, bool two_rows, int n, const W& w,
                           double t, double* scratch, double* incl_s /* [kThreads] */, int* iscratch) {
     constexpr int E = D::E;
-    const int nvec = (n + E - 1) / E;
-    const bool fast = pair_aligned<D>(rp, rq, two_rows);
-    double vs[kMaxScanRounds];
-#pragma unroll
-    for (int j = 0; j < kMaxScanRounds; ++j) {
-        const int v = j * kThreads + threadIdx.x;
-        vs[j] = 0.0;
-        if (v < nvec) {
-            float a[E];
-            vector_weights<D>(rp, rq, two_rows, fast, v, n, w, a);
-#pragma unroll
-            for (int e = 0; e < E; ++e) vs[j] += (double)a[e];
-        }
-    }
+    constexpr int U = kScanVec;
     __shared__ int result;
-    if (threadIdx.x == 0) result = -1;
-    double run = 0.0;
-    int last_pos_vec = -1;  // this thread's last vector with positive weight
+    const int tid = threadIdx.x;
+    const bool fast = pair_aligned<D>(rp, rq, two_rows);
+    float a[U][E];
+    double sum = 0.0;
+    {
+        float zp[U][E], zq[U][E];
+        load_pair_u<D, U>(rp, rq, two_rows, fast, tid * U, 1, n, zp, zq);
 #pragma unroll
-    for (int j = 0; j < kMaxScanRounds; ++j) {
-        if (j * kThreads >= nvec) break;
-        const int v = j * kThreads + threadIdx.x;
-        if (vs[j] > 0.0) last_pos_vec = v;
-        double tot;
-        const double incl = block_inclusive_scan(vs[j], scratch, &tot);
-        incl_s[threadIdx.x] = incl;
-        const int first = block_first(v < nvec && run + incl > t, iscratch);
-        if (first < kThreads) {
-            if ((int)threadIdx.x == first) {
-                float a[E];
-                vector_weights<D>(rp, rq, two_rows, fast, v, n, w, a);
-                double cum = run + (first == 0 ? 0.0 : incl_s[first - 1]);
-                int idx = -1, lastp = -1;
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                a[u][e] = w(zp[u][e], zq[u][e]);
+                sum += (double)a[u][e];
+            }
+    }
+    if (tid == 0) result = -1;
+    double tot;
+    const double incl = block_inclusive_scan(sum, scratch, &tot);
+    incl_s[tid] = incl;
+    const int first = block_first(incl > t, iscratch);
+    if (first < kThreads) {
+        if (tid == first) {
+            double cum = (first == 0) ? 0.0 : incl_s[first - 1];
+            int idx = -1, lastp = -1;
+#pragma unroll
+            for (int u = 0; u < U; ++u)
 #pragma unroll
                 for (int e = 0; e < E; ++e) {
-                    if (a[e] > 0.0f) lastp = e;
-                    cum += (double)a[e];
-                    if (idx < 0 && cum > t && a[e] > 0.0f) idx = e;
+                    if (a[u][e] > 0.0f) lastp = u * E + e;
+                    cum += (double)a[u][e];
+                    if (idx < 0 && cum > t && a[u][e] > 0.0f) idx = u * E + e;
                 }
-                if (idx < 0) idx = lastp;
-                result = (idx >= 0) ? v * E + idx : -1;
-            }
-            __syncthreads();
-            return result;
+            if (idx < 0) idx = lastp;
+            result = (idx >= 0) ? tid * U * E + idx : -1;
         }
-        run += tot;
-        __syncthreads();
-    }
-    // t lies at or beyond the chunk total (rounding only): take the last positive weight.
-    const int lv = wave_max_int(last_pos_vec);
-    __syncthreads();
-    if ((threadIdx.x % kWave) == 0) iscratch[threadIdx.x / kWave] = lv;
-    __syncthreads();
-    int best = -1;
-    for (int i = 0; i < kWaves; ++i) best = max(best, iscratch[i]);
-    if (best >= 0 && (int)threadIdx.x == best % kThreads) {
-        float a[E];
-        vector_weights<D>(rp, rq, two_rows, fast, best, n, w, a);
+    } else {
+        // t lies at or beyond the chunk total (rounding only): the last positive weight
         int lastp = -1;
 #pragma unroll
-        for (int e = 0; e < E; ++e)
-            if (a[e] > 0.0f) lastp = e;
-        result = (lastp >= 0) ? best * E + lastp : -1;
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                if (a[u][e] > 0.0f) lastp = tid * U * E + u * E + e;
+        const int lv = wave_max_int(lastp);
+        if ((tid % kWave) == 0) iscratch[tid / kWave] = lv;
+        __syncthreads();
+        if (tid == 0) {
+            int best = -1;
+            for (int i = 0; i < kWaves; ++i) best = max(best, iscratch[i]);
+            result = best;
+        }
     }
     __syncthreads();
     return result;
@@ -321,7 +357,14 @@ __global__ __launch_bounds__(kThreads) void row_stats_kernel(const typename D::T
 }
 
 // ---------------------------------------------------------------------------
-// pass 2 (both modes): decisions, final-distribution chunk masses, the draw
+// pass 2 (both modes): the decision and the final-distribution chunk masses
+// pass 3 (both modes): the inverse-CDF draw
+//
+// Workgroups never wait on each other inside a kernel: on this multi-XCD part
+// every device-scope release/acquire is an L2 writeback/invalidate, which
+// costs far more than a kernel boundary.  Every pass-2 workgroup of a batch
+// element therefore recomputes the (cheap) decision itself, and the draw is
+// a separate launch.
 // ---------------------------------------------------------------------------
 struct SelectParams {
     const void* draft;
@@ -336,7 +379,7 @@ struct SelectParams {
     double temperature, alpha, beta;
     const RowPartial* partial;
     double* chunk_mass;        // [B, nchunk2]
-    unsigned int* ticket;      // [B], zero between calls
+    struct Selection* sel;     // [B]
     int32_t* accepted_len;
     int32_t* next_token;
     double* tau_out;           // optional probes
@@ -345,62 +388,88 @@ struct SelectParams {
     double* lognorm_out;
 };
 
+// The decision for one batch element, as pass 3 needs it.
+struct Selection {
+    int L;      // accepted length, in [0, gamma]
+    int bad;    // 1: sentinel
+    ExactWeights ew;
+    SigmoidWeights sw;
+};
+
+constexpr int kMergeCap = 1024;  // row-normaliser partials staged in LDS at once
+
 __device__ __forceinline__ double min1(double r) { return (r >= 1.0) ? 1.0 : r; }  // keeps NaN
 
 template <class D, bool kExact>
-__global__ __launch_bounds__(kThreads) void select_sample_kernel(SelectParams P) {
+__global__ __launch_bounds__(kThreads) void mass_kernel(SelectParams P) {
     using T = typename D::T;
     __shared__ float rowK[kExact ? kMaxRows : 1];
     __shared__ double rowS[kExact ? kMaxRows : 1];
+    __shared__ float pk[kExact ? kMergeCap : 1];
+    __shared__ double ps[kExact ? kMergeCap : 1];
     __shared__ double tau_s[kMaxGamma];
     __shared__ int stop_s[kMaxGamma];
     __shared__ double scratch[kWaves];
-    __shared__ double incl_s[kThreads];
-    __shared__ int iscratch[kWaves];
-    __shared__ int sel_L, sel_bad, tok_bad, is_last, fin_chunk;
-    __shared__ double fin_total, fin_t;
+    __shared__ int sel_L, sel_bad, tok_bad;
 
     const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
     const int b = blockIdx.x / P.nchunk2;
     const int k2 = blockIdx.x - b * P.nchunk2;
     const T* draft = static_cast<const T*>(P.draft) + (size_t)b * gamma * V;
     const T* target = static_cast<const T*>(P.target) + (size_t)b * (gamma + 1) * V;
-    const int wave = threadIdx.x / kWave;
-    const int lane = threadIdx.x % kWave;
+    const int tid = threadIdx.x;
 
-    if (threadIdx.x == 0) tok_bad = 0;
-    // row normalisers of b, merged in a fixed order (every workgroup of b
-    // computes identical values)
+    // independent loads first: tokens and uniforms, then the drafted-token
+    // logits (their latency overlaps the normaliser merge below)
+    int x = 0;
+    double r = 0.0;
+    bool tok_ok = true;
+    float zp = 0.0f, zq = 0.0f;
+    if (tid == 0) tok_bad = 0;
+    if (tid < gamma) {
+        x = P.tokens[(size_t)b * gamma + tid];
+        r = (double)P.uniforms[(size_t)b * (gamma + 1) + tid];
+        tok_ok = (x >= 0 && x < V);
+        const int xs = tok_ok ? x : 0;
+        zp = to_f32(target[(size_t)tid * V + xs]);
+        zq = to_f32(draft[(size_t)tid * V + xs]);
+    }
+
+    // row normalisers of b: partials staged in LDS by groups of rows, each row
+    // merged sequentially in chunk order (identical in every workgroup of b,
+    // and identical for draft and target rows with equal values)
     if (kExact) {
-        const RowPartial* pb = P.partial + (size_t)b * R * P.nchunk1;
-        for (int r = wave; r < R; r += kWaves) {
-            Lse st{-INFINITY, 0.0};
-            for (int k = lane; k < P.nchunk1; k += kWave) {
-                const RowPartial p = pb[(size_t)r * P.nchunk1 + k];
-                st = lse_merge(st, Lse{p.k, p.s});
+        const int nc1 = P.nchunk1;
+        const RowPartial* pb = P.partial + (size_t)b * R * nc1;
+        const int G = max(1, kMergeCap / nc1);
+        for (int r0 = 0; r0 < R; r0 += G) {
+            const int r1 = min(R, r0 + G);
+            const int np = (r1 - r0) * nc1;
+            __syncthreads();
+            for (int i = tid; i < np; i += kThreads) {
+                const RowPartial q = pb[(size_t)r0 * nc1 + i];
+                pk[i] = q.k;
+                ps[i] = q.s;
             }
-            const Lse w = wave_lse(st);
-            if (lane == 0) {
-                rowK[r] = w.k;
-                rowS[r] = w.s;
+            __syncthreads();
+            if (tid < r1 - r0) {
+                Lse st{-INFINITY, 0.0};
+                for (int k = 0; k < nc1; ++k) st = lse_merge(st, Lse{pk[tid * nc1 + k], ps[tid * nc1 + k]});
+                rowK[r0 + tid] = st.k;
+                rowS[r0 + tid] = st.s;
             }
         }
     }
     __syncthreads();
 
     // eq. (1) at the drafted tokens
-    for (int c = threadIdx.x; c < gamma; c += kThreads) {
-        const int x = P.tokens[(size_t)b * gamma + c];
-        const bool tok_ok = (x >= 0 && x < V);
+    if (tid < gamma) {
         if (!tok_ok) tok_bad = 1;
-        const int xs = tok_ok ? x : 0;
-        const float zp = to_f32(target[(size_t)c * V + xs]);
-        const float zq = to_f32(draft[(size_t)c * V + xs]);
         double tau;
         bool row_ok;
         if (kExact) {
-            const double lam_p = (double)rowK[c] + log2(rowS[c]);
-            const double lam_q = (double)rowK[gamma + 1 + c] + log2(rowS[gamma + 1 + c]);
+            const double lam_p = (double)rowK[tid] + log2(rowS[tid]);
+            const double lam_q = (double)rowK[gamma + 1 + tid] + log2(rowS[gamma + 1 + tid]);
             row_ok = isfinite(lam_p) && isfinite(lam_q);
             if (zq == -INFINITY) {
                 tau = 1.0;  // q(x) = 0
@@ -417,12 +486,11 @@ __global__ __launch_bounds__(kThreads) void select_sample_kernel(SelectParams P)
             tau = (qh > 0.0) ? min1(ph / qh) : 1.0;
             row_ok = isfinite(tau);
         }
-        const bool accept = (double)P.uniforms[(size_t)b * (gamma + 1) + c] <= tau;
-        tau_s[c] = tau;
-        stop_s[c] = !row_ok ? 2 : (accept ? 0 : 1);
+        tau_s[tid] = tau;
+        stop_s[tid] = !row_ok ? 2 : ((r <= tau) ? 0 : 1);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
         int L = gamma, bad = tok_bad;
         for (int c = 0; c < gamma; ++c) {
             if (stop_s[c] != 0) {
@@ -441,19 +509,8 @@ __global__ __launch_bounds__(kThreads) void select_sample_kernel(SelectParams P)
     __syncthreads();
     const int L = sel_L;
     const bool bad = sel_bad != 0;
-
-    if (k2 == 0) {
-        if (P.tau_out != nullptr)
-            for (int c = threadIdx.x; c < gamma; c += kThreads) P.tau_out[(size_t)b * gamma + c] = tau_s[c];
-        if (kExact && P.lognorm_out != nullptr)
-            for (int r = threadIdx.x; r < R; r += kThreads)
-                P.lognorm_out[(size_t)b * R + r] = ((double)rowK[r] + log2(rowS[r])) * 0.693147180559945309417;
-    }
-
-    // the weights of the distribution the next token is drawn from
     const bool two_rows = L < gamma;
-    const T* rp = target + (size_t)min(L, gamma) * V;
-    const T* rq = draft + (size_t)min(L, gamma - 1) * V;
+
     ExactWeights ew{};
     SigmoidWeights sw{};
     if (kExact && !bad) {
@@ -477,48 +534,83 @@ __global__ __launch_bounds__(kThreads) void select_sample_kernel(SelectParams P)
         sw.s0 = P.s0;
     }
 
+    if (k2 == 0) {
+        if (tid == 0) {
+            Selection sel;
+            sel.L = L;
+            sel.bad = bad ? 1 : 0;
+            sel.ew = ew;
+            sel.sw = sw;
+            P.sel[b] = sel;
+        }
+        if (P.tau_out != nullptr && tid < gamma) P.tau_out[(size_t)b * gamma + tid] = tau_s[tid];
+        if (kExact && P.lognorm_out != nullptr)
+            for (int i = tid; i < R; i += kThreads)
+                P.lognorm_out[(size_t)b * R + i] = ((double)rowK[i] + log2(rowS[i])) * 0.693147180559945309417;
+    }
+
+    // this workgroup's chunk of the final distribution
+    const T* rp = target + (size_t)min(L, gamma) * V;
+    const T* rq = draft + (size_t)min(L, gamma - 1) * V;
     const int begin = k2 * P.chunk2;
     const int n = min(V, begin + P.chunk2) - begin;
-    float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V : nullptr;
+    float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V + begin : nullptr;
     double m = 0.0;
     if (!bad) {
         if (kExact)
-            m = chunk_weight_sum<D>(rp + begin, rq + begin, two_rows, n, ew, wrow ? wrow + begin : nullptr, scratch);
+            m = chunk_weight_sum<D>(rp + begin, rq + begin, two_rows, n, ew, wrow, scratch);
         else
-            m = chunk_weight_sum<D>(rp + begin, rq + begin, two_rows, n, sw, wrow ? wrow + begin : nullptr, scratch);
+            m = chunk_weight_sum<D>(rp + begin, rq + begin, two_rows, n, sw, wrow, scratch);
     }
-    if (threadIdx.x == 0) P.chunk_mass[(size_t)b * P.nchunk2 + k2] = m;
+    if (tid == 0) P.chunk_mass[(size_t)b * P.nchunk2 + k2] = m;
+}
 
-    // completion counter: the last workgroup of b performs the draw
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const unsigned int prev = atomicAdd(&P.ticket[b], 1u);
-        is_last = (prev == (unsigned int)(P.nchunk2 - 1));
-    }
-    __syncthreads();
-    if (!is_last) return;
-    __threadfence();
-    if (threadIdx.x == 0) P.ticket[b] = 0u;
+constexpr int kMaxChunks2 = 1024;
 
-    if (bad) {
-        if (threadIdx.x == 0) {
+template <class D, bool kExact>
+__global__ __launch_bounds__(kThreads) void draw_kernel(SelectParams P) {
+    using T = typename D::T;
+    __shared__ double cm[kMaxChunks2];
+    __shared__ double scratch[kWaves];
+    __shared__ double incl_s[kThreads];
+    __shared__ int iscratch[kWaves];
+    __shared__ int fin_chunk;
+    __shared__ double fin_total, fin_t;
+
+    const int gamma = P.gamma, V = P.V;
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x;
+    const Selection sel = P.sel[b];
+    for (int k = tid; k < P.nchunk2; k += kThreads) cm[k] = P.chunk_mass[(size_t)b * P.nchunk2 + k];
+    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
+    if (sel.bad) {
+        if (tid == 0) {
             P.accepted_len[b] = -1;
             P.next_token[b] = -1;
             if (P.mass_out != nullptr) P.mass_out[b] = __builtin_nan("");
         }
         return;
     }
-    const double* cm = P.chunk_mass + (size_t)b * P.nchunk2;
-    if (threadIdx.x == 0) {
+    const int L = sel.L;
+    const T* target = static_cast<const T*>(P.target) + (size_t)b * (gamma + 1) * V;
+    const T* draft = static_cast<const T*>(P.draft) + (size_t)b * gamma * V;
+    const T* rp = target + (size_t)min(L, gamma) * V;
+    const T* rq = draft + (size_t)min(L, gamma - 1) * V;
+    ExactWeights ew = sel.ew;
+    SigmoidWeights sw = sel.sw;
+    bool two_rows = L < gamma;
+    float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V : nullptr;
+
+    __syncthreads();
+    if (tid == 0) {
         double tot = 0.0;
         for (int k = 0; k < P.nchunk2; ++k) tot += cm[k];
         fin_total = tot;
     }
     __syncthreads();
-    bool fallback = two_rows && fin_total == 0.0;
-    if (fallback) {
-        // no residual mass (sigmoid mode): draw from target row L instead
+    if (two_rows && fin_total == 0.0) {
+        // no residual mass (possible in sigmoid mode): draw from target row L
+        two_rows = false;
         ew.kind = kTargetRow;
         sw.kind = kTargetRow;
         for (int k = 0; k < P.nchunk2; ++k) {
@@ -526,11 +618,10 @@ __global__ __launch_bounds__(kThreads) void select_sample_kernel(SelectParams P)
             const int nk = min(V, bk + P.chunk2) - bk;
             const double mk = kExact ? chunk_weight_sum<D>(rp + bk, rq + bk, false, nk, ew, wrow ? wrow + bk : nullptr, scratch)
                                      : chunk_weight_sum<D>(rp + bk, rq + bk, false, nk, sw, wrow ? wrow + bk : nullptr, scratch);
-            if (threadIdx.x == 0) P.chunk_mass[(size_t)b * P.nchunk2 + k] = mk;
+            if (tid == 0) cm[k] = mk;
         }
-        __threadfence_block();
         __syncthreads();
-        if (threadIdx.x == 0) {
+        if (tid == 0) {
             double tot = 0.0;
             for (int k = 0; k < P.nchunk2; ++k) tot += cm[k];
             fin_total = tot;
@@ -539,20 +630,20 @@ __global__ __launch_bounds__(kThreads) void select_sample_kernel(SelectParams P)
     }
     const double total = fin_total;
     if (!(isfinite(total) && total > 0.0)) {
-        if (threadIdx.x == 0) {
+        if (tid == 0) {
             P.accepted_len[b] = -1;
             P.next_token[b] = -1;
             if (P.mass_out != nullptr) P.mass_out[b] = total;
         }
         return;
     }
-    if (threadIdx.x == 0) {
-        const double t = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma] * total;
+    if (tid == 0) {
+        const double t = u * total;
         double cum = 0.0;
         int j = -1, lastpos = 0;
         for (int k = 0; k < P.nchunk2; ++k) {
             if (cm[k] > 0.0) lastpos = k;
-            if (j < 0 && cum + cm[k] > t) {
+            if (cum + cm[k] > t) {
                 j = k;
                 break;
             }
@@ -566,13 +657,11 @@ __global__ __launch_bounds__(kThreads) void select_sample_kernel(SelectParams P)
     const int j = fin_chunk;
     const int bj = j * P.chunk2;
     const int nj = min(V, bj + P.chunk2) - bj;
-    const bool rows2 = two_rows && !fallback;
-    const int idx = kExact ? chunk_find<D>(rp + bj, rq + bj, rows2, nj, ew, fin_t, scratch, incl_s, iscratch)
-                           : chunk_find<D>(rp + bj, rq + bj, rows2, nj, sw, fin_t, scratch, incl_s, iscratch);
-    if (threadIdx.x == 0) {
-        P.accepted_len[b] = L;
+    const int idx = kExact ? chunk_find<D>(rp + bj, rq + bj, two_rows, nj, ew, fin_t, scratch, incl_s, iscratch)
+                           : chunk_find<D>(rp + bj, rq + bj, two_rows, nj, sw, fin_t, scratch, incl_s, iscratch);
+    if (tid == 0) {
+        P.accepted_len[b] = (idx >= 0) ? L : -1;
         P.next_token[b] = (idx >= 0) ? bj + idx : -1;
-        if (idx < 0) P.accepted_len[b] = -1;
         if (P.mass_out != nullptr) P.mass_out[b] = total;
     }
 }
@@ -589,7 +678,7 @@ struct Plan {
     int E;
     int chunk1, nchunk1;
     int chunk2, nchunk2;
-    size_t off_partial, off_mass, off_ticket, bytes;
+    size_t off_partial, off_mass, off_sel, bytes;
 };
 
 static inline long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
@@ -615,7 +704,7 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     p->nchunk1 = (int)ceil_div(V, chunk);
     if ((long long)B * R * p->nchunk1 > 0x7fffffffLL) return false;
 
-    const long long max_scan = (long long)kMaxScanRounds * kThreads * E;  // in-chunk scan capacity
+    const long long max_scan = (long long)kScanVec * kThreads * E;  // in-chunk scan capacity
     long long nc2 = ceil_div(kWantSampleTiles, B);
     nc2 = std::max(nc2, ceil_div(V, kSampleTileBytes / s));
     nc2 = std::min(nc2, max_cells);
@@ -626,9 +715,10 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     if ((long long)B * p->nchunk2 > 0x7fffffffLL) return false;
     p->E = E;
 
+    if (p->nchunk2 > kMaxChunks2) return false;
     size_t off = 0;
-    p->off_ticket = off;
-    off = align256(off + sizeof(uint32_t) * (size_t)B);
+    p->off_sel = off;
+    off = align256(off + sizeof(Selection) * (size_t)B);
     p->off_mass = off;
     off = align256(off + sizeof(double) * (size_t)B * p->nchunk2);
     p->off_partial = off;
@@ -683,7 +773,7 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.s0 = (float)(-(double)a.alpha / ((double)a.beta - (double)a.alpha));
     P.partial = partial;
     P.chunk_mass = reinterpret_cast<double*>(ws + pl.off_mass);
-    P.ticket = reinterpret_cast<unsigned int*>(ws + pl.off_ticket);
+    P.sel = reinterpret_cast<Selection*>(ws + pl.off_sel);
     P.accepted_len = a.accepted_len;
     P.next_token = a.next_token;
     P.tau_out = a.tau_out;
@@ -695,9 +785,11 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
         const int tiles = a.B * (2 * a.gamma + 1) * pl.nchunk1;
         hipLaunchKernelGGL(row_stats_kernel<D>, dim3(tiles), dim3(kThreads), 0, a.stream, draft, target, a.gamma,
                            a.V, pl.chunk1, pl.nchunk1, P.c, partial);
-        hipLaunchKernelGGL((select_sample_kernel<D, true>), dim3(a.B * pl.nchunk2), dim3(kThreads), 0, a.stream, P);
+        hipLaunchKernelGGL((mass_kernel<D, true>), dim3(a.B * pl.nchunk2), dim3(kThreads), 0, a.stream, P);
+        hipLaunchKernelGGL((draw_kernel<D, true>), dim3(a.B), dim3(kThreads), 0, a.stream, P);
     } else {
-        hipLaunchKernelGGL((select_sample_kernel<D, false>), dim3(a.B * pl.nchunk2), dim3(kThreads), 0, a.stream, P);
+        hipLaunchKernelGGL((mass_kernel<D, false>), dim3(a.B * pl.nchunk2), dim3(kThreads), 0, a.stream, P);
+        hipLaunchKernelGGL((draw_kernel<D, false>), dim3(a.B), dim3(kThreads), 0, a.stream, P);
     }
     return hipGetLastError() == hipSuccess ? SV_OK : SV_ERR_HIP;
 }
