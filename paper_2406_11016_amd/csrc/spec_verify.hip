@@ -84,8 +84,9 @@ struct ExactWeights {
     float kp, lp_hi, lp_lo;  // target row: reference k and log2(s) as hi + lo
     float kq, lq_hi, lq_lo;  // draft row
     float d_hi, d_lo;        // Lambda_p - Lambda_q as hi + lo
-    __device__ __forceinline__ float operator()(float zp, float zq) const {
-        if (kind == kTargetRow) return exp2_hw((fmaf(zp, c, -kp) - lp_hi) - lp_lo);
+    template <int KIND>
+    __device__ __forceinline__ float eval(float zp, float zq) const {
+        if (KIND == kTargetRow) return exp2_hw((fmaf(zp, c, -kp) - lp_hi) - lp_lo);
         float dz, dz_lo;
         two_diff(zp, zq, dz, dz_lo);
         const float d = fmaf(dz_lo, c, fmaf(dz, c, -d_hi)) - d_lo;
@@ -107,9 +108,10 @@ __device__ __forceinline__ float sigm(float x) {
 struct SigmoidWeights {
     int kind;
     float s, s0;  // u = fma(z, s, s0)
-    __device__ __forceinline__ float operator()(float zp, float zq) const {
+    template <int KIND>
+    __device__ __forceinline__ float eval(float zp, float zq) const {
         const float up = fmaf(zp, s, s0);
-        if (kind == kTargetRow) return sigm(up);
+        if (KIND == kTargetRow) return sigm(up);
         if (zp != zp || zq != zq) return __builtin_nanf("");
         float dz, dz_lo;
         two_diff(zp, zq, dz, dz_lo);
@@ -138,33 +140,33 @@ __device__ __forceinline__ void load_pair_u(const typename D::T* rp, const typen
                                             float (&zq)[U][D::E]) {
     constexpr int E = D::E;
     const int nfull = n / E;
-    if (fast) {
+    if (fast && nfull > 0) {
         u32x4 a[U], c[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int v = v0 + u * vstride;
-            if (v < nfull) {
-                a[u] = load16<D>(rp + v * E);
-                if (two_rows) c[u] = load16<D>(rq + v * E);
-            }
+            a[u] = load_vec_or_pad<D, false>(rp, v0 + u * vstride, nfull);
+            if (two_rows) c[u] = load_vec_or_pad<D, false>(rq, v0 + u * vstride, nfull);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
+            unpack<D>(a[u], zp[u]);
+            if (two_rows) unpack<D>(c[u], zq[u]);
+        }
+        // the partial vector at the end of a row, if this thread holds it
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
             const int v = v0 + u * vstride;
-            if (v < nfull) {
-                unpack<D>(a[u], zp[u]);
-                if (two_rows) unpack<D>(c[u], zq[u]);
-            } else {
-                load_elems<D>(rp, v * E, n, -INFINITY, zp[u]);
-                if (two_rows) load_elems<D>(rq, v * E, n, -INFINITY, zq[u]);
+            if (v == nfull && nfull * E < n) {
+                load_elems_or_pad<D>(rp, v * E, n, zp[u]);
+                if (two_rows) load_elems_or_pad<D>(rq, v * E, n, zq[u]);
             }
         }
     } else {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int v = v0 + u * vstride;
-            load_elems<D>(rp, v * E, n, -INFINITY, zp[u]);
-            if (two_rows) load_elems<D>(rq, v * E, n, -INFINITY, zq[u]);
+            load_elems_or_pad<D>(rp, v * E, n, zp[u]);
+            if (two_rows) load_elems_or_pad<D>(rq, v * E, n, zq[u]);
         }
     }
     if (!two_rows) {
@@ -179,10 +181,11 @@ constexpr int kPassUnroll = 4;  // vectors per thread per round in the weight pa
 
 // Sum of the weights over one chunk (rp/rq point at the chunk start, n
 // elements); optionally stores every weight.  Valid in every thread.
-template <class D, class W>
-__device__ double chunk_weight_sum(const typename D::T* rp, const typename D::T* rq, bool two_rows, int n,
-                                   const W& w, float* wout, double* scratch) {
+template <class D, int KIND, class W>
+__device__ __forceinline__ double chunk_weight_sum_k(const typename D::T* rp, const typename D::T* rq, int n,
+                                                     const W& w, float* wout, double* scratch) {
     constexpr int E = D::E;
+    constexpr bool two_rows = (KIND == kResidual);
     const int nvec = (n + E - 1) / E;
     const bool fast = pair_aligned<D>(rp, rq, two_rows);
     double acc = 0.0;
@@ -195,13 +198,20 @@ __device__ double chunk_weight_sum(const typename D::T* rp, const typename D::T*
             if (v >= nvec) continue;
 #pragma unroll
             for (int e = 0; e < E; ++e) {
-                const float a = w(zp[u][e], zq[u][e]);
+                const float a = w.template eval<KIND>(zp[u][e], zq[u][e]);
                 if (wout != nullptr && v * E + e < n) wout[v * E + e] = a;
                 acc += (double)a;
             }
         }
     }
     return block_sum(acc, scratch);
+}
+
+template <class D, class W>
+__device__ double chunk_weight_sum(const typename D::T* rp, const typename D::T* rq, int n, const W& w,
+                                   float* wout, double* scratch) {
+    return (w.kind == kTargetRow) ? chunk_weight_sum_k<D, kTargetRow>(rp, rq, n, w, wout, scratch)
+                                  : chunk_weight_sum_k<D, kResidual>(rp, rq, n, w, wout, scratch);
 }
 
 // Lowest thread index whose predicate holds, or kThreads.  Valid in every thread.
@@ -223,10 +233,12 @@ __device__ __forceinline__ int block_first(bool pred, int* iscratch /* [kWaves] 
 // chunk total at or below t.  Valid in every thread.  Thread i owns the
 // contiguous vectors [i * kScanVec, (i + 1) * kScanVec), so one workgroup scan
 // of the per-thread sums follows element order.  Needs n <= kScanVec * kThreads * E.
-template <class D, class W>
-__device__ int chunk_find(const typename D::T* rp, const typename D::T* rq, bool two_rows, int n, const W& w,
-                          double t, double* scratch, double* incl_s /* [kThreads] */, int* iscratch) {
+template <class D, int KIND, class W>
+__device__ __forceinline__ int chunk_find_k(const typename D::T* rp, const typename D::T* rq, int n, const W& w,
+                                            double t, double* scratch, double* incl_s /* [kThreads] */,
+                                            int* iscratch) {
     constexpr int E = D::E;
+    constexpr bool two_rows = (KIND == kResidual);
     constexpr int U = kScanVec;
     __shared__ int result;
     const int tid = threadIdx.x;
@@ -240,7 +252,7 @@ __device__ int chunk_find(const typename D::T* rp, const typename D::T* rq, bool
         for (int u = 0; u < U; ++u)
 #pragma unroll
             for (int e = 0; e < E; ++e) {
-                a[u][e] = w(zp[u][e], zq[u][e]);
+                a[u][e] = w.template eval<KIND>(zp[u][e], zq[u][e]);
                 sum += (double)a[u][e];
             }
     }
@@ -285,6 +297,13 @@ __device__ int chunk_find(const typename D::T* rp, const typename D::T* rq, bool
     return result;
 }
 
+template <class D, class W>
+__device__ int chunk_find(const typename D::T* rp, const typename D::T* rq, int n, const W& w, double t,
+                          double* scratch, double* incl_s, int* iscratch) {
+    return (w.kind == kTargetRow) ? chunk_find_k<D, kTargetRow>(rp, rq, n, w, t, scratch, incl_s, iscratch)
+                                  : chunk_find_k<D, kResidual>(rp, rq, n, w, t, scratch, incl_s, iscratch);
+}
+
 // ---------------------------------------------------------------------------
 // exact mode, pass 1: per-chunk row normalisers
 // ---------------------------------------------------------------------------
@@ -309,48 +328,40 @@ __global__ __launch_bounds__(kThreads) void row_stats_kernel(const typename D::T
     const int begin = k * chunk;
     const int n = min(V, begin + chunk) - begin;
     const T* base = row + begin;
-    const int nfull = n / E;
+    const int nfull = n / E;            // whole 16-byte vectors
+    const int nvec = (n + E - 1) / E;   // plus a partial one at the end of a row
+    const bool aligned = (reinterpret_cast<uintptr_t>(base) & 15u) == 0;
 
+    // Thread t takes whole vectors t, t + kThreads, ... in blocks of kUnroll;
+    // all loads of a block are issued before any is used, and the block shares
+    // one update of the running reference.  A partial vector at the end of a
+    // row is absorbed after the loop by the thread that would own it.  The
+    // assignment and order depend only on element indices, never on the
+    // row's address, so equal rows give bit-identical normalisers.
     Lse st{-INFINITY, 0.0};
-    if ((reinterpret_cast<uintptr_t>(base) & 15u) == 0) {
+    if (nfull > 0) {
         for (int v0 = 0; v0 < nfull; v0 += kUnroll * kThreads) {
-            u32x4 raw[kUnroll];
+            float x[kUnroll][E];
+            if (aligned) {
+                u32x4 raw[kUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int v = v0 + u * kThreads + threadIdx.x;
-                if (v < nfull) raw[u] = load16<D>(base + v * E);
-            }
+                for (int u = 0; u < kUnroll; ++u)
+                    raw[u] = load_vec_or_pad<D, true>(base, v0 + u * kThreads + (int)threadIdx.x, nfull);
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int v = v0 + u * kThreads + threadIdx.x;
-                if (v < nfull) {
-                    float x[E];
-                    unpack<D>(raw[u], x);
-                    lse_absorb<E>(st, x, c);
-                }
-            }
-        }
-    } else {
-        // rows that are not 16-byte aligned (e.g. odd V in fp32): same
-        // element-to-thread assignment, element-wise loads
-        for (int v0 = 0; v0 < nfull; v0 += kUnroll * kThreads) {
-            float xs[kUnroll][E];
+                for (int u = 0; u < kUnroll; ++u) unpack<D>(raw[u], x[u]);
+            } else {
+                // rows that are not 16-byte aligned (e.g. odd V in fp32)
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int v = v0 + u * kThreads + threadIdx.x;
-                if (v < nfull) load_elems<D>(base, v * E, n, -INFINITY, xs[u]);
+                for (int u = 0; u < kUnroll; ++u)
+                    load_elems_or_pad<D>(base, (v0 + u * kThreads + (int)threadIdx.x) * E, nfull * E, x[u]);
             }
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int v = v0 + u * kThreads + threadIdx.x;
-                if (v < nfull) lse_absorb<E>(st, xs[u], c);
-            }
+            lse_absorb_block<kUnroll, E>(st, x, c);
         }
     }
-    if (n % E != 0 && (int)threadIdx.x == nfull % kThreads) {
-        float x[E];
-        load_elems<D>(base, nfull * E, n, -INFINITY, x);
-        lse_absorb<E>(st, x, c);
+    if (nvec > nfull && (int)threadIdx.x == nfull % kThreads) {
+        float x[1][E];
+        load_elems_or_pad<D>(base, nfull * E, n, x[0]);
+        lse_absorb_block<1, E>(st, x, c);
     }
     const Lse blk = block_lse(st, sk, ss);
     if (threadIdx.x == 0) partial[tile] = RowPartial{blk.s, blk.k, 0.0f};
@@ -558,9 +569,9 @@ __global__ __launch_bounds__(kThreads) void mass_kernel(SelectParams P) {
     double m = 0.0;
     if (!bad) {
         if (kExact)
-            m = chunk_weight_sum<D>(rp + begin, rq + begin, two_rows, n, ew, wrow, scratch);
+            m = chunk_weight_sum<D>(rp + begin, rq + begin, n, ew, wrow, scratch);
         else
-            m = chunk_weight_sum<D>(rp + begin, rq + begin, two_rows, n, sw, wrow, scratch);
+            m = chunk_weight_sum<D>(rp + begin, rq + begin, n, sw, wrow, scratch);
     }
     if (tid == 0) P.chunk_mass[(size_t)b * P.nchunk2 + k2] = m;
 }
@@ -616,8 +627,8 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(SelectParams P) {
         for (int k = 0; k < P.nchunk2; ++k) {
             const int bk = k * P.chunk2;
             const int nk = min(V, bk + P.chunk2) - bk;
-            const double mk = kExact ? chunk_weight_sum<D>(rp + bk, rq + bk, false, nk, ew, wrow ? wrow + bk : nullptr, scratch)
-                                     : chunk_weight_sum<D>(rp + bk, rq + bk, false, nk, sw, wrow ? wrow + bk : nullptr, scratch);
+            const double mk = kExact ? chunk_weight_sum<D>(rp + bk, rq + bk, nk, ew, wrow ? wrow + bk : nullptr, scratch)
+                                     : chunk_weight_sum<D>(rp + bk, rq + bk, nk, sw, wrow ? wrow + bk : nullptr, scratch);
             if (tid == 0) cm[k] = mk;
         }
         __syncthreads();
@@ -657,8 +668,8 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(SelectParams P) {
     const int j = fin_chunk;
     const int bj = j * P.chunk2;
     const int nj = min(V, bj + P.chunk2) - bj;
-    const int idx = kExact ? chunk_find<D>(rp + bj, rq + bj, two_rows, nj, ew, fin_t, scratch, incl_s, iscratch)
-                           : chunk_find<D>(rp + bj, rq + bj, two_rows, nj, sw, fin_t, scratch, incl_s, iscratch);
+    const int idx = kExact ? chunk_find<D>(rp + bj, rq + bj, nj, ew, fin_t, scratch, incl_s, iscratch)
+                           : chunk_find<D>(rp + bj, rq + bj, nj, sw, fin_t, scratch, incl_s, iscratch);
     if (tid == 0) {
         P.accepted_len[b] = (idx >= 0) ? L : -1;
         P.next_token[b] = (idx >= 0) ? bj + idx : -1;

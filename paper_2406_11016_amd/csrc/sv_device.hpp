@@ -86,13 +86,36 @@ __device__ __forceinline__ u32x4 load16(const typename D::T* p) {
     return *reinterpret_cast<const u32x4*>(p);
 }
 
-// Elements i..i+E-1 of a row with element-wise loads (any alignment); indices
-// at or beyond `end` read as `pad`.
+// A 16-byte vector whose every element is -inf in storage type D.
 template <class D>
-__device__ __forceinline__ void load_elems(const typename D::T* row, int i, int end, float pad,
-                                           float (&x)[D::E]) {
+__device__ __forceinline__ u32x4 neg_inf_vec();
+template <>
+__device__ __forceinline__ u32x4 neg_inf_vec<F32>() { return u32x4{0xff800000u, 0xff800000u, 0xff800000u, 0xff800000u}; }
+template <>
+__device__ __forceinline__ u32x4 neg_inf_vec<F16>() { return u32x4{0xfc00fc00u, 0xfc00fc00u, 0xfc00fc00u, 0xfc00fc00u}; }
+template <>
+__device__ __forceinline__ u32x4 neg_inf_vec<BF16>() { return u32x4{0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u}; }
+
+// Vector v of a 16-byte aligned chunk holding nfull (>= 1) whole vectors, or
+// the -inf vector when v >= nfull.  The load is unconditional (its index is
+// clamped into range) so that a block of such loads is issued back to back.
+template <class D, bool NT>
+__device__ __forceinline__ u32x4 load_vec_or_pad(const typename D::T* base, int v, int nfull) {
+    const u32x4* p = reinterpret_cast<const u32x4*>(base + (size_t)min(v, nfull - 1) * D::E);
+    const u32x4 r = NT ? __builtin_nontemporal_load(p) : *p;
+    return (v < nfull) ? r : neg_inf_vec<D>();
+}
+
+// Elements i..i+E-1 of a chunk of n (>= 1) elements with element-wise loads
+// (any alignment); indices at or beyond n read as -inf.  Loads are
+// unconditional (clamped indices), so they issue back to back.
+template <class D>
+__device__ __forceinline__ void load_elems_or_pad(const typename D::T* base, int i, int n, float (&x)[D::E]) {
 #pragma unroll
-    for (int e = 0; e < D::E; ++e) x[e] = (i + e < end) ? to_f32(row[i + e]) : pad;
+    for (int e = 0; e < D::E; ++e) {
+        const float val = to_f32(base[min(i + e, n - 1)]);
+        x[e] = (i + e < n) ? val : -INFINITY;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -175,25 +198,38 @@ __device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
     return Lse{k, ldexp(a.s, exp_delta(a.k - k)) + ldexp(b.s, exp_delta(b.k - k))};
 }
 
-template <int E>
-__device__ __forceinline__ void lse_absorb(Lse& st, const float (&x)[E], float c) {
-    float m = x[0];
+// Absorb a block of U vectors with one update of the reference: the block's
+// maximum first, then its terms summed pairwise in fp32 and added to the fp64
+// running sum once.
+template <int U, int E>
+__device__ __forceinline__ void lse_absorb_block(Lse& st, const float (&x)[U][E], float c) {
+    float m = x[0][0];
 #pragma unroll
-    for (int e = 1; e < E; ++e) m = fmaxf(m, x[e]);
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int e = 0; e < E; ++e) m = fmaxf(m, x[u][e]);
     const float kv = ceilf(m * c);
     if (kv > st.k) {
         st.s = ldexp(st.s, exp_delta(st.k - kv));
         st.k = kv;
     }
     const float nk = (st.k == -INFINITY) ? 0.0f : -st.k;
-    float t[E];
+    float t[U];
 #pragma unroll
-    for (int e = 0; e < E; ++e) t[e] = __builtin_amdgcn_exp2f(fmaf(x[e], c, nk));
+    for (int u = 0; u < U; ++u) {
+        float v[E];
 #pragma unroll
-    for (int w = E / 2; w >= 1; w /= 2) {
+        for (int e = 0; e < E; ++e) v[e] = __builtin_amdgcn_exp2f(fmaf(x[u][e], c, nk));
 #pragma unroll
-        for (int e = 0; e < w; ++e) t[e] += t[e + w];
+        for (int w = E / 2; w >= 1; w /= 2)
+#pragma unroll
+            for (int e = 0; e < w; ++e) v[e] += v[e + w];
+        t[u] = v[0];
     }
+#pragma unroll
+    for (int w = U / 2; w >= 1; w /= 2)
+#pragma unroll
+        for (int u = 0; u < w; ++u) t[u] += t[u + w];
     st.s += (double)t[0];
 }
 
