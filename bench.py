@@ -41,6 +41,32 @@ def algorithmic_bytes(w) -> int:
     return w.batch * (2 * w.gamma * s + 2 * w.vocab * s) + small
 
 
+def source_hash() -> str:
+    """sha256 prefix of the kernel sources (to match recorded counter data)."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2406_11016_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(workload: str):
+    """HBM bytes per launch from the recorded rocprofv3 counter runs, or None
+    if none were recorded for this workload or the kernel changed since."""
+    path = os.path.join(ROOT, "profiles", "verify_kernel_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_hash") != source_hash():
+        return None
+    w = rec.get("workloads", {}).get(workload)
+    return None if w is None else int(w["traffic_bytes"])
+
+
 def cpu_baseline(w, x, min_seconds: float):
     """The oracle as it stands, timed on a bounded sample of the same inputs."""
     import numpy as np
@@ -158,9 +184,9 @@ def main() -> int:
     alg = algorithmic_bytes(w)
     achieved = alg / (ms_per_step * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
-                "kernel": "whole step (row_stats_kernel + mass_kernel + draw_kernel)" if w.mode == "exact"
-                else "whole step (mass_kernel + draw_kernel)", "algorithmic_bytes_per_step": alg}
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": recorded_traffic(w.name),
+                "kernel": "verify_kernel<exact> (the whole step is one launch)" if w.mode == "exact"
+                else "verify_kernel<sigmoid> (the whole step is one launch)", "algorithmic_bytes_per_step": alg}
 
     cpu = None
     if not args.no_cpu_baseline:

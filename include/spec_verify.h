@@ -43,11 +43,12 @@
  * library never allocates, frees, synchronises or prints.  Inputs are only
  * read; outputs and the workspace are overwritten.  A call enqueues its
  * kernels on `stream` and returns without waiting: SV_OK means "launched".
- * The workspace needs no initialisation (every byte a call reads was written
- * earlier in the same call).  Calls that share a workspace must be ordered
- * (same stream, or synchronised); concurrent calls need separate workspaces.
- * There is no mutable global state: the functions are reentrant and
- * thread-safe.
+ * The workspace must be zero-filled once before its first use (for example
+ * with spec_verify_workspace_init); every call leaves it zero-filled again.
+ * It carries the hand-off between the workgroups of the single launch a call
+ * makes.  Calls that share a workspace must be ordered (same stream, or
+ * synchronised); concurrent calls need separate workspaces.  There is no
+ * mutable global state: the functions are reentrant and thread-safe.
  *
  * Errors.  Invalid arguments are detected on the host before anything is
  * launched and return a negative status.  Bad data found on the device --
@@ -95,16 +96,19 @@ typedef enum sv_status {
 
 /*
  * Bytes of device workspace a call with these sizes needs (the same value
- * serves both modes).  Returns 0 for invalid sizes.  The workspace holds the
- * per-chunk row normalisers (exact mode), the per-batch-element decision and
- * the per-chunk masses of the final distribution.
+ * serves both modes).  Returns 0 for invalid sizes, including vocabularies
+ * above 2^20 (fp32) or 2^21 (fp16 / bf16) entries.  The workspace holds the
+ * per-chunk row log-normalisers (exact mode) and the per-chunk masses of the
+ * final distribution.  The 32-bit word at byte offset 4 becomes nonzero if a
+ * wait between workgroups ever times out (about 0.1 s), which would indicate
+ * a fault; results of that call are sentinels and the workspace must be
+ * re-initialised.
  */
 size_t spec_verify_workspace_bytes(int32_t batch, int32_t gamma, int32_t vocab, sv_dtype_t dtype);
 
 /*
  * Zero-fills `workspace_bytes` bytes of `workspace` on `stream` with a fill
- * kernel (no memset node, so the call may be captured in a graph).  Optional:
- * the verification calls do not depend on the workspace's prior contents.
+ * kernel (no memset node, so the call may be captured in a graph).
  */
 sv_status_t spec_verify_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
 

@@ -101,9 +101,10 @@ def _stream(device) -> ctypes.c_void_p:
 
 
 def new_workspace(batch: int, gamma: int, vocab: int, dtype, device) -> torch.Tensor:
-    """A workspace for these sizes (reusable across ordered calls; needs no initialisation)."""
+    """A zero-filled workspace for these sizes (reusable across ordered calls;
+    each call leaves it zero-filled)."""
     n = workspace_bytes(batch, gamma, vocab, dtype)
-    return torch.empty((n + 15) // 16 * 16, dtype=torch.uint8, device=device)
+    return torch.zeros((n + 15) // 16 * 16, dtype=torch.uint8, device=device)
 
 
 def init_workspace(ws: torch.Tensor) -> None:
@@ -147,8 +148,8 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
     """One verification step on the current stream.
 
     Returns ``(accepted_len, next_token)`` (int32 [B] device tensors), plus a
-    :class:`Probe` when ``probe`` is true.  ``workspace`` may be passed to
-    avoid an allocation per call.
+    :class:`Probe` when ``probe`` is true.  ``workspace`` (zero-filled before
+    its first use) may be passed to avoid an allocation per call.
     """
     if mode not in ("exact", "sigmoid"):
         raise ValueError(mode)

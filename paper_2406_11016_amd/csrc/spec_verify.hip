@@ -2,25 +2,23 @@
 //
 // Method: arXiv 2406.11016, Sec. 3.1 (eqs. (1)-(3)) and Sec. 3.2.2 (eqs. (4)-(5)).
 //
-// Exact mode, three launches on the caller's stream:
-//   row_stats_kernel  grid = B * (2*gamma+1) * nchunk1 workgroups.  Each
-//                     streams one chunk of one logit row exactly once with
-//                     128-bit loads and writes that chunk's contribution to
-//                     the row's softmax normaliser (eq. (4)).  This kernel
-//                     moves every logit byte and bounds the step.
-//   mass_kernel       grid = B * nchunk2.  Every workgroup of batch element b
-//                     merges b's chunk normalisers in a fixed order, evaluates
-//                     tau_c (eq. (1)) at the drafted tokens and runs the
-//                     first-rejection scan, so all of them agree on L without
-//                     communicating; each then sums the weights a(x) of the
-//                     final distribution (residual of eqs. (2)-(3), or target
-//                     row gamma) over its chunk of the selected row(s).
-//   draw_kernel       grid = B.  Fixed-order prefix over b's chunk masses,
-//                     then a workgroup scan inside the chunk the uniform falls
-//                     in: the inverse-CDF draw of the next token.
-// Sigmoid mode: mass_kernel and draw_kernel only; the element-wise
-// approximation of eq. (5) needs no row normaliser, so only the logits at the
-// drafted tokens and the row(s) the next token is drawn from are read.
+// One launch per call.  Workgroups play one of four roles by index (see
+// verify_kernel):
+//   stats    (exact mode) one chunk of one logit row, streamed once with
+//            128-bit non-temporal loads: the chunk's contribution to the row's
+//            softmax normaliser (eq. (4)).  These move every logit byte and
+//            bound the step.
+//   decider  b: tau_c of eq. (1) at the drafted tokens and the
+//            first-rejection scan for batch element b, made once.
+//   mass     (b, tile): the weights a(x) of the final distribution (residual
+//            of eqs. (2)-(3), or target row gamma) summed over the tile, one
+//            sub-chunk per wave.
+//   draw     b: fixed-order prefix over b's sub-chunk masses, then one
+//            workgroup scan inside the sub-chunk the uniform falls in -- the
+//            inverse-CDF draw of the next token.
+// Sigmoid mode (eq. (5)) has no stats role: it needs no row normaliser, so
+// only the logits at the drafted tokens and the row(s) the next token is
+// drawn from are read.
 #include <math.h>
 #include <stdint.h>
 
@@ -34,7 +32,6 @@ namespace sv {
 
 enum : int { kResidual = 0, kTargetRow = 1 };
 
-constexpr int kScanVec = 4;              // contiguous vectors per thread in the in-chunk scan
 constexpr int kWantStatsTiles = 2048;    // enough workgroups to fill 256 CUs several times
 constexpr int kWantSampleTiles = 1024;
 constexpr int kStatsTileBytes = 65536;   // at most 64 KiB of one row per stats workgroup
@@ -177,41 +174,152 @@ __device__ __forceinline__ void load_pair_u(const typename D::T* rp, const typen
     }
 }
 
-constexpr int kPassUnroll = 4;  // vectors per thread per round in the weight pass
+constexpr int kPassUnroll = 4;  // vectors in flight per lane in the weight pass
+constexpr int kMergeCap = 1024;  // chunk log-normalisers of one batch element (2 gamma + 1 rows)
+constexpr int kMaxSub = 1024;    // sub-chunk masses of one batch element (nchunk2 * kWaves)
+constexpr int kMaxSpins = 1 << 17;  // bound on every wait (about 0.1 s), so every wave exits
+constexpr int kDecisionWords = 5;          // L and the sentinel flag, then 8 floats of weight constants
 
-// Sum of the weights over one chunk (rp/rq point at the chunk start, n
-// elements); optionally stores every weight.  Valid in every thread.
+// ---------------------------------------------------------------------------
+// results passed between workgroups of one launch
+//
+// A result is one fp64 value published as one 64-bit word with a relaxed,
+// agent-scope atomic store, bit-inverted so that the all-zero word means
+// "not yet published" (NaN is canonicalised first, so no value maps to zero).
+// Since every result is a single word, readers need no fence: on this
+// multi-XCD part a device-scope release/acquire is an L2 writeback and
+// invalidate, far costlier than the spin on a word.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ unsigned long long encode_word(double v) {
+    if (v != v) v = __builtin_nan("");
+    return ~(unsigned long long)__double_as_longlong(v);
+}
+__device__ __forceinline__ double decode_word(unsigned long long w) { return __longlong_as_double((long long)~w); }
+__device__ __forceinline__ void publish(unsigned long long* p, double v) {
+    __hip_atomic_store(p, encode_word(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void clear_word(unsigned long long* p) {
+    __hip_atomic_store(p, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// A raw 64-bit record word (never all ones), published the same way.
+__device__ __forceinline__ void publish_raw(unsigned long long* p, unsigned long long v) {
+    __hip_atomic_store(p, ~v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long pack2(float a, float b) {
+    const unsigned int ua = (a != a) ? 0x7fc00000u : __float_as_uint(a);  // canonical NaN
+    const unsigned int ub = (b != b) ? 0x7fc00000u : __float_as_uint(b);
+    return ((unsigned long long)ua << 32) | ub;
+}
+__device__ __forceinline__ float unpack_hi(unsigned long long w) { return __uint_as_float((unsigned int)(w >> 32)); }
+__device__ __forceinline__ float unpack_lo(unsigned long long w) { return __uint_as_float((unsigned int)w); }
+
+// Waits until the n raw words at p are published and copies them to dst.
+__device__ __forceinline__ bool wait_raw(unsigned long long* p, int n, unsigned long long* dst) {
+    for (int spin = 0;; ++spin) {
+        int missing = 0;
+        for (int i = threadIdx.x; i < n; i += kThreads) {
+            const unsigned long long w = __hip_atomic_load(p + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (w == 0ull)
+                missing = 1;
+            else
+                dst[i] = ~w;
+        }
+        if (__syncthreads_or(missing) == 0) return true;
+        if (spin >= kMaxSpins) return false;
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
+// Waits until the n words at p are published and copies them, decoded, to
+// dst (LDS).  Called by every thread; returns false after kMaxSpins polls.
+__device__ __forceinline__ bool wait_words(unsigned long long* p, int n, double* dst) {
+    for (int spin = 0;; ++spin) {
+        int missing = 0;
+        for (int i = threadIdx.x; i < n; i += kThreads) {
+            const unsigned long long w = __hip_atomic_load(p + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (w == 0ull)
+                missing = 1;
+            else
+                dst[i] = decode_word(w);
+        }
+        if (__syncthreads_or(missing) == 0) return true;
+        if (spin >= kMaxSpins) return false;
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// the final-distribution pass: tile k2 of the selected row(s) covers elements
+// [k2 * chunk2, min(V, (k2 + 1) * chunk2)); wave w of the tile covers the
+// contiguous sub-chunk of vectors [w * q, (w + 1) * q), q = ceil(chunk2 / E / kWaves).
+// Each sub-chunk mass is published; the draw scans one sub-chunk (q <= kThreads).
+// ---------------------------------------------------------------------------
+struct Span {
+    int begin;  // first element, relative to the row
+    int n;      // number of elements (may be 0)
+};
+
+__device__ __forceinline__ Span sub_chunk(int k2, int w, int chunk2, int V, int E) {
+    const int q = (chunk2 / E + kWaves - 1) / kWaves;
+    const int tb = k2 * chunk2;
+    const int tn = min(V, tb + chunk2) - tb;
+    const int b0 = min(tn, w * q * E);
+    const int b1 = min(tn, (w + 1) * q * E);
+    return Span{tb + b0, b1 - b0};
+}
+
+// Sum of the weights over one sub-chunk by one wave (rp/rq at the sub-chunk
+// start, n elements); optionally stores every weight.  Valid in every lane.
+// Lanes take vectors lane, lane + 64, ...; kPassUnroll 16-byte loads per row
+// are in flight per lane, kept raw and unpacked one vector at a time.
 template <class D, int KIND, class W>
-__device__ __forceinline__ double chunk_weight_sum_k(const typename D::T* rp, const typename D::T* rq, int n,
-                                                     const W& w, float* wout, double* scratch) {
+__device__ __forceinline__ double wave_weight_sum_k(const typename D::T* rp, const typename D::T* rq, int n,
+                                                    const W& w, float* wout) {
     constexpr int E = D::E;
     constexpr bool two_rows = (KIND == kResidual);
+    const int lane = threadIdx.x % kWave;
     const int nvec = (n + E - 1) / E;
-    const bool fast = pair_aligned<D>(rp, rq, two_rows);
+    const int nfull = n / E;
+    const bool fast = pair_aligned<D>(rp, rq, two_rows) && nfull > 0;
     double acc = 0.0;
-    for (int v0 = 0; v0 < nvec; v0 += kPassUnroll * kThreads) {
-        float zp[kPassUnroll][E], zq[kPassUnroll][E];
-        load_pair_u<D, kPassUnroll>(rp, rq, two_rows, fast, v0 + (int)threadIdx.x, kThreads, n, zp, zq);
+    for (int v0 = 0; v0 < nvec; v0 += kPassUnroll * kWave) {
+        u32x4 ra[kPassUnroll], rb[kPassUnroll];
+        if (fast) {
+#pragma unroll
+            for (int u = 0; u < kPassUnroll; ++u) {
+                ra[u] = load_vec_or_pad<D, false>(rp, v0 + u * kWave + lane, nfull);
+                if (two_rows) rb[u] = load_vec_or_pad<D, false>(rq, v0 + u * kWave + lane, nfull);
+            }
+        }
 #pragma unroll
         for (int u = 0; u < kPassUnroll; ++u) {
-            const int v = v0 + u * kThreads + (int)threadIdx.x;
+            const int v = v0 + u * kWave + lane;
             if (v >= nvec) continue;
+            float zp[E], zq[E];
+            if (fast && v < nfull) {
+                unpack<D>(ra[u], zp);
+                if (two_rows) unpack<D>(rb[u], zq);
+            } else {
+                load_elems_or_pad<D>(rp, v * E, n, zp);
+                if (two_rows) load_elems_or_pad<D>(rq, v * E, n, zq);
+            }
 #pragma unroll
             for (int e = 0; e < E; ++e) {
-                const float a = w.template eval<KIND>(zp[u][e], zq[u][e]);
+                const float a = w.template eval<KIND>(zp[e], two_rows ? zq[e] : -INFINITY);
                 if (wout != nullptr && v * E + e < n) wout[v * E + e] = a;
                 acc += (double)a;
             }
         }
     }
-    return block_sum(acc, scratch);
+    return wave_sum(acc);
 }
 
 template <class D, class W>
-__device__ double chunk_weight_sum(const typename D::T* rp, const typename D::T* rq, int n, const W& w,
-                                   float* wout, double* scratch) {
-    return (w.kind == kTargetRow) ? chunk_weight_sum_k<D, kTargetRow>(rp, rq, n, w, wout, scratch)
-                                  : chunk_weight_sum_k<D, kResidual>(rp, rq, n, w, wout, scratch);
+__device__ double wave_weight_sum(const typename D::T* rp, const typename D::T* rq, int n, const W& w,
+                                  float* wout) {
+    return (w.kind == kTargetRow) ? wave_weight_sum_k<D, kTargetRow>(rp, rq, n, w, wout)
+                                  : wave_weight_sum_k<D, kResidual>(rp, rq, n, w, wout);
 }
 
 // Lowest thread index whose predicate holds, or kThreads.  Valid in every thread.
@@ -228,35 +336,28 @@ __device__ __forceinline__ int block_first(bool pred, int* iscratch /* [kWaves] 
     return f;
 }
 
-// Index (relative to the chunk start) of the first element whose running
+// Index (relative to the sub-chunk start) of the first element whose running
 // weight sum exceeds t, or of the last positive weight if rounding leaves the
-// chunk total at or below t.  Valid in every thread.  Thread i owns the
-// contiguous vectors [i * kScanVec, (i + 1) * kScanVec), so one workgroup scan
-// of the per-thread sums follows element order.  Needs n <= kScanVec * kThreads * E.
+// sub-chunk total at or below t.  Thread i holds vector i (n <= kThreads * E),
+// so one workgroup scan follows element order.  Valid in every thread.
 template <class D, int KIND, class W>
-__device__ __forceinline__ int chunk_find_k(const typename D::T* rp, const typename D::T* rq, int n, const W& w,
-                                            double t, double* scratch, double* incl_s /* [kThreads] */,
-                                            int* iscratch) {
+__device__ __forceinline__ int sub_chunk_find_k(const typename D::T* rp, const typename D::T* rq, int n,
+                                                const W& w, double t, double* scratch, double* incl_s,
+                                                int* iscratch, int* result) {
     constexpr int E = D::E;
     constexpr bool two_rows = (KIND == kResidual);
-    constexpr int U = kScanVec;
-    __shared__ int result;
     const int tid = threadIdx.x;
     const bool fast = pair_aligned<D>(rp, rq, two_rows);
-    float a[U][E];
+    float zp[1][E], zq[1][E];
+    load_pair_u<D, 1>(rp, rq, two_rows, fast, tid, 1, n, zp, zq);
+    float a[E];
     double sum = 0.0;
-    {
-        float zp[U][E], zq[U][E];
-        load_pair_u<D, U>(rp, rq, two_rows, fast, tid * U, 1, n, zp, zq);
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                a[u][e] = w.template eval<KIND>(zp[u][e], zq[u][e]);
-                sum += (double)a[u][e];
-            }
+    for (int e = 0; e < E; ++e) {
+        a[e] = w.template eval<KIND>(zp[0][e], zq[0][e]);
+        sum += (double)a[e];
     }
-    if (tid == 0) result = -1;
+    if (tid == 0) *result = -1;
     double tot;
     const double incl = block_inclusive_scan(sum, scratch, &tot);
     incl_s[tid] = incl;
@@ -266,65 +367,125 @@ __device__ __forceinline__ int chunk_find_k(const typename D::T* rp, const typen
             double cum = (first == 0) ? 0.0 : incl_s[first - 1];
             int idx = -1, lastp = -1;
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    if (a[u][e] > 0.0f) lastp = u * E + e;
-                    cum += (double)a[u][e];
-                    if (idx < 0 && cum > t && a[u][e] > 0.0f) idx = u * E + e;
-                }
+            for (int e = 0; e < E; ++e) {
+                if (a[e] > 0.0f) lastp = e;
+                cum += (double)a[e];
+                if (idx < 0 && cum > t && a[e] > 0.0f) idx = e;
+            }
             if (idx < 0) idx = lastp;
-            result = (idx >= 0) ? tid * U * E + idx : -1;
+            *result = (idx >= 0) ? tid * E + idx : -1;
         }
     } else {
-        // t lies at or beyond the chunk total (rounding only): the last positive weight
+        // t lies at or beyond the sub-chunk total (rounding only): the last positive weight
         int lastp = -1;
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                if (a[u][e] > 0.0f) lastp = tid * U * E + u * E + e;
+        for (int e = 0; e < E; ++e)
+            if (a[e] > 0.0f) lastp = tid * E + e;
         const int lv = wave_max_int(lastp);
         if ((tid % kWave) == 0) iscratch[tid / kWave] = lv;
         __syncthreads();
         if (tid == 0) {
             int best = -1;
             for (int i = 0; i < kWaves; ++i) best = max(best, iscratch[i]);
-            result = best;
+            *result = best;
         }
     }
     __syncthreads();
-    return result;
+    return *result;
 }
 
 template <class D, class W>
-__device__ int chunk_find(const typename D::T* rp, const typename D::T* rq, int n, const W& w, double t,
-                          double* scratch, double* incl_s, int* iscratch) {
-    return (w.kind == kTargetRow) ? chunk_find_k<D, kTargetRow>(rp, rq, n, w, t, scratch, incl_s, iscratch)
-                                  : chunk_find_k<D, kResidual>(rp, rq, n, w, t, scratch, incl_s, iscratch);
+__device__ int sub_chunk_find(const typename D::T* rp, const typename D::T* rq, int n, const W& w, double t,
+                              double* scratch, double* incl_s, int* iscratch, int* result) {
+    return (w.kind == kTargetRow) ? sub_chunk_find_k<D, kTargetRow>(rp, rq, n, w, t, scratch, incl_s, iscratch, result)
+                                  : sub_chunk_find_k<D, kResidual>(rp, rq, n, w, t, scratch, incl_s, iscratch, result);
 }
 
 // ---------------------------------------------------------------------------
-// exact mode, pass 1: per-chunk row normalisers
+// the fused step: one launch; a workgroup's role follows from its index
+//   stats (b, r, k)  exact mode: chunk k of row r of batch element b -> the
+//                    chunk's log-normaliser (eq. (4)), published
+//   decider (b)      b's decision -- eq. (1) at the drafted tokens and the
+//                    first-rejection scan -- published as a small record
+//   mass (b, k2)     the masses of the final distribution (eqs. (2)-(3) or
+//                    the bonus row) over tile k2, one per wave, published
+//   draw (b)         the inverse-CDF draw of b's next token; clears b's
+//                    published words for the next call
+// Index order runs over blocks j = 0, 1, ...; block j holds the stats tiles
+// of b = j, the decider of b = j - lag[0], the mass tiles of b = j - lag[1]
+// and the draw of b = j - lag[2], so each role of b comes after the roles it
+// reads and the lags let the stream of later batch elements cover the
+// latency of earlier ones.  A workgroup only waits on results of workgroups
+// with smaller indices, and never on a returning atomic: the streaming
+// workgroups publish and retire.  Each XCD dispatches its workgroups in index
+// order, so the waiting workgroup with the smallest index always waits on
+// workgroups that are running and do not wait, or that its XCD will dispatch
+// once its running, non-waiting workgroups finish: no wait can block forever.
+// Every wait is also bounded (kMaxSpins), so every wave exits regardless.
 // ---------------------------------------------------------------------------
+struct StepParams {
+    const void* draft;
+    const void* target;
+    const int32_t* tokens;
+    const float* uniforms;
+    int B, gamma, V;
+    int chunk1, nchunk1;           // exact: row chunks
+    int chunk2, nchunk2;           // final-distribution tiles per batch element
+    int n_stats, n_mass, n_total;  // workgroups by role
+    int lag[3];                    // block lags of the decider, mass and draw roles
+    float c;                       // exact: log2(e) / T
+    float s, s0;                   // sigmoid: u = fma(z, s, s0)
+    double temperature, alpha, beta;
+    unsigned int* error;           // set to 1 if a wait ever timed out
+    unsigned long long* dslot;     // [B, kDecisionWords] the published decision (exact mode)
+    unsigned long long* pslot;     // [B, 2 gamma + 1, nchunk1] chunk log2-normalisers
+    unsigned long long* mslot;     // [B, nchunk2, kWaves] sub-chunk masses
+    int32_t* accepted_len;
+    int32_t* next_token;
+    double* tau_out;               // optional probes
+    float* weight_out;
+    double* mass_out;
+    double* lognorm_out;
+};
+
+struct Smem {
+    double words[kMergeCap];   // exact: b's chunk log2-normalisers
+    double rowL[kMaxRows];     // exact: b's row log2-normalisers
+    double tau[kMaxGamma];
+    int stop[kMaxGamma];
+    double sub[kMaxSub];       // draw: b's sub-chunk masses
+    double incl[kThreads];
+    double scratch[kWaves];
+    int iscratch[kWaves];
+    float sk[kWaves];
+    double ss[kWaves];
+    unsigned long long rec[kDecisionWords];
+    int L, bad, tok_bad, timed_out, result, cross, last;
+    double cross_t;
+};
+
+__device__ __forceinline__ double min1(double r) { return (r >= 1.0) ? 1.0 : r; }  // keeps NaN
+
+__device__ __forceinline__ void split3(double v, float& hi, float& mid, float& lo) {
+    hi = (float)v;
+    mid = (float)(v - (double)hi);
+    lo = (float)((v - (double)hi) - (double)mid);
+}
+
+// Exact mode, one chunk of one row: sum_x 2^(z c - k) in one streaming pass,
+// published as the chunk's log2-normaliser k + log2(s).
 template <class D>
-__global__ __launch_bounds__(kThreads) void row_stats_kernel(const typename D::T* __restrict__ draft,
-                                                             const typename D::T* __restrict__ target, int gamma,
-                                                             int V, int chunk, int nchunk, float c,
-                                                             RowPartial* __restrict__ partial) {
+__device__ __forceinline__ void stats_role(const StepParams& P, int tile, Smem& sm) {
     using T = typename D::T;
     constexpr int E = D::E;
-    __shared__ float sk[kWaves];
-    __shared__ double ss[kWaves];
-
-    const int R = 2 * gamma + 1;
-    const int tile = blockIdx.x;
+    const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1, nchunk = P.nchunk1, chunk = P.chunk1;
+    const float c = P.c;
     const int k = tile % nchunk;
     const int rowid = tile / nchunk;  // b * R + r
     const int b = rowid / R;
     const int r = rowid - b * R;
-    const T* row = (r <= gamma) ? target + ((size_t)b * (gamma + 1) + r) * (size_t)V
-                                : draft + ((size_t)b * gamma + (r - gamma - 1)) * (size_t)V;
+    const T* row = (r <= gamma) ? static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + r) * (size_t)V
+                                : static_cast<const T*>(P.draft) + ((size_t)b * gamma + (r - gamma - 1)) * (size_t)V;
     const int begin = k * chunk;
     const int n = min(V, begin + chunk) - begin;
     const T* base = row + begin;
@@ -363,80 +524,35 @@ __global__ __launch_bounds__(kThreads) void row_stats_kernel(const typename D::T
         load_elems_or_pad<D>(base, nfull * E, n, x[0]);
         lse_absorb_block<1, E>(st, x, c);
     }
-    const Lse blk = block_lse(st, sk, ss);
-    if (threadIdx.x == 0) partial[tile] = RowPartial{blk.s, blk.k, 0.0f};
+    const Lse blk = block_lse(st, sm.sk, sm.ss);
+    if (threadIdx.x == 0) publish(P.pslot + tile, (double)blk.k + log2(blk.s));
 }
 
-// ---------------------------------------------------------------------------
-// pass 2 (both modes): the decision and the final-distribution chunk masses
-// pass 3 (both modes): the inverse-CDF draw
-//
-// Workgroups never wait on each other inside a kernel: on this multi-XCD part
-// every device-scope release/acquire is an L2 writeback/invalidate, which
-// costs far more than a kernel boundary.  Every pass-2 workgroup of a batch
-// element therefore recomputes the (cheap) decision itself, and the draw is
-// a separate launch.
-// ---------------------------------------------------------------------------
-struct SelectParams {
-    const void* draft;
-    const void* target;
-    const int32_t* tokens;
-    const float* uniforms;
-    int B, gamma, V;
-    int nchunk1;               // exact: chunks per row in `partial`
-    int chunk2, nchunk2;       // chunking of the final-distribution pass
-    float c;                   // exact: log2(e) / T
-    float s, s0;               // sigmoid: u = fma(z, s, s0)
-    double temperature, alpha, beta;
-    const RowPartial* partial;
-    double* chunk_mass;        // [B, nchunk2]
-    struct Selection* sel;     // [B]
-    int32_t* accepted_len;
-    int32_t* next_token;
-    double* tau_out;           // optional probes
-    float* weight_out;
-    double* mass_out;
-    double* lognorm_out;
-};
-
-// The decision for one batch element, as pass 3 needs it.
-struct Selection {
-    int L;      // accepted length, in [0, gamma]
-    int bad;    // 1: sentinel
+struct Decision {
+    int L;        // accepted length, in [0, gamma]
+    bool bad;     // sentinel
+    bool ok;      // false if a wait timed out
     ExactWeights ew;
     SigmoidWeights sw;
 };
 
-constexpr int kMergeCap = 1024;  // row-normaliser partials staged in LDS at once
-
-__device__ __forceinline__ double min1(double r) { return (r >= 1.0) ? 1.0 : r; }  // keeps NaN
-
+// The decision for batch element b: eq. (1) at the drafted tokens and the
+// first-rejection scan, plus the weights of the final distribution.  Every
+// workgroup that needs it computes it the same way, so they all agree.
 template <class D, bool kExact>
-__global__ __launch_bounds__(kThreads) void mass_kernel(SelectParams P) {
+__device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
-    __shared__ float rowK[kExact ? kMaxRows : 1];
-    __shared__ double rowS[kExact ? kMaxRows : 1];
-    __shared__ float pk[kExact ? kMergeCap : 1];
-    __shared__ double ps[kExact ? kMergeCap : 1];
-    __shared__ double tau_s[kMaxGamma];
-    __shared__ int stop_s[kMaxGamma];
-    __shared__ double scratch[kWaves];
-    __shared__ int sel_L, sel_bad, tok_bad;
-
     const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
-    const int b = blockIdx.x / P.nchunk2;
-    const int k2 = blockIdx.x - b * P.nchunk2;
+    const int tid = threadIdx.x;
     const T* draft = static_cast<const T*>(P.draft) + (size_t)b * gamma * V;
     const T* target = static_cast<const T*>(P.target) + (size_t)b * (gamma + 1) * V;
-    const int tid = threadIdx.x;
 
-    // independent loads first: tokens and uniforms, then the drafted-token
-    // logits (their latency overlaps the normaliser merge below)
+    // independent loads first: tokens, uniforms and the drafted-token logits
     int x = 0;
     double r = 0.0;
     bool tok_ok = true;
     float zp = 0.0f, zq = 0.0f;
-    if (tid == 0) tok_bad = 0;
+    if (tid == 0) sm.tok_bad = 0;
     if (tid < gamma) {
         x = P.tokens[(size_t)b * gamma + tid];
         r = (double)P.uniforms[(size_t)b * (gamma + 1) + tid];
@@ -446,41 +562,35 @@ __global__ __launch_bounds__(kThreads) void mass_kernel(SelectParams P) {
         zq = to_f32(draft[(size_t)tid * V + xs]);
     }
 
-    // row normalisers of b: partials staged in LDS by groups of rows, each row
-    // merged sequentially in chunk order (identical in every workgroup of b,
-    // and identical for draft and target rows with equal values)
+    Decision d{};
+    d.ok = true;
     if (kExact) {
+        // b's chunk log2-normalisers, then each row's, merged in chunk order
         const int nc1 = P.nchunk1;
-        const RowPartial* pb = P.partial + (size_t)b * R * nc1;
-        const int G = max(1, kMergeCap / nc1);
-        for (int r0 = 0; r0 < R; r0 += G) {
-            const int r1 = min(R, r0 + G);
-            const int np = (r1 - r0) * nc1;
-            __syncthreads();
-            for (int i = tid; i < np; i += kThreads) {
-                const RowPartial q = pb[(size_t)r0 * nc1 + i];
-                pk[i] = q.k;
-                ps[i] = q.s;
+        d.ok = wait_words(P.pslot + (size_t)b * R * nc1, R * nc1, sm.words);
+        for (int i = tid; i < R; i += kThreads) {
+            double m = -INFINITY;
+            bool nan = false;
+            for (int k = 0; k < nc1; ++k) {
+                const double l = sm.words[i * nc1 + k];
+                nan |= (l != l);
+                m = fmax(m, l);
             }
-            __syncthreads();
-            if (tid < r1 - r0) {
-                Lse st{-INFINITY, 0.0};
-                for (int k = 0; k < nc1; ++k) st = lse_merge(st, Lse{pk[tid * nc1 + k], ps[tid * nc1 + k]});
-                rowK[r0 + tid] = st.k;
-                rowS[r0 + tid] = st.s;
-            }
+            double sum = 0.0;
+            if (!nan && m != -INFINITY)
+                for (int k = 0; k < nc1; ++k) sum += exp2(sm.words[i * nc1 + k] - m);
+            sm.rowL[i] = nan ? __builtin_nan("") : ((m == -INFINITY) ? -INFINITY : m + log2(sum));
         }
     }
     __syncthreads();
 
-    // eq. (1) at the drafted tokens
     if (tid < gamma) {
-        if (!tok_ok) tok_bad = 1;
+        if (!tok_ok) sm.tok_bad = 1;
         double tau;
         bool row_ok;
         if (kExact) {
-            const double lam_p = (double)rowK[tid] + log2(rowS[tid]);
-            const double lam_q = (double)rowK[gamma + 1 + tid] + log2(rowS[gamma + 1 + tid]);
+            const double lam_p = sm.rowL[tid];
+            const double lam_q = sm.rowL[gamma + 1 + tid];
             row_ok = isfinite(lam_p) && isfinite(lam_q);
             if (zq == -INFINITY) {
                 tau = 1.0;  // q(x) = 0
@@ -497,184 +607,288 @@ __global__ __launch_bounds__(kThreads) void mass_kernel(SelectParams P) {
             tau = (qh > 0.0) ? min1(ph / qh) : 1.0;
             row_ok = isfinite(tau);
         }
-        tau_s[tid] = tau;
-        stop_s[tid] = !row_ok ? 2 : ((r <= tau) ? 0 : 1);
+        sm.tau[tid] = tau;
+        sm.stop[tid] = !row_ok ? 2 : ((r <= tau) ? 0 : 1);
     }
     __syncthreads();
     if (tid == 0) {
-        int L = gamma, bad = tok_bad;
+        int L = gamma, bad = sm.tok_bad;
         for (int c = 0; c < gamma; ++c) {
-            if (stop_s[c] != 0) {
+            if (sm.stop[c] != 0) {
                 L = c;
-                if (stop_s[c] == 2) bad = 1;
+                if (sm.stop[c] == 2) bad = 1;
                 break;
             }
         }
-        if (kExact && !bad && L == gamma) {
-            const double lam = (double)rowK[gamma] + log2(rowS[gamma]);
-            if (!isfinite(lam)) bad = 1;
-        }
-        sel_L = L;
-        sel_bad = bad;
+        if (kExact && !bad && L == gamma && !isfinite(sm.rowL[gamma])) bad = 1;
+        sm.L = L;
+        sm.bad = bad;
     }
     __syncthreads();
-    const int L = sel_L;
-    const bool bad = sel_bad != 0;
-    const bool two_rows = L < gamma;
-
-    ExactWeights ew{};
-    SigmoidWeights sw{};
-    if (kExact && !bad) {
-        const int rpi = min(L, gamma), rqi = gamma + 1 + min(L, gamma - 1);
-        const double lp = log2(rowS[rpi]), lq = log2(rowS[rqi]);
-        const double dl = ((double)rowK[rpi] + lp) - ((double)rowK[rqi] + lq);
-        ew.kind = two_rows ? kResidual : kTargetRow;
-        ew.c = P.c;
-        ew.kp = rowK[rpi];
-        ew.lp_hi = (float)lp;
-        ew.lp_lo = (float)(lp - (double)ew.lp_hi);
-        ew.kq = rowK[rqi];
-        ew.lq_hi = (float)lq;
-        ew.lq_lo = (float)(lq - (double)ew.lq_hi);
-        ew.d_hi = (float)dl;
-        ew.d_lo = (float)(dl - (double)ew.d_hi);
+    d.L = sm.L;
+    d.bad = sm.bad != 0 || !d.ok;
+    const bool two_rows = d.L < gamma;
+    if (kExact && !d.bad) {
+        const double lp = sm.rowL[min(d.L, gamma)];
+        const double lq = sm.rowL[gamma + 1 + min(d.L, gamma - 1)];
+        d.ew.kind = two_rows ? kResidual : kTargetRow;
+        d.ew.c = P.c;
+        split3(lp, d.ew.kp, d.ew.lp_hi, d.ew.lp_lo);
+        split3(lq, d.ew.kq, d.ew.lq_hi, d.ew.lq_lo);
+        float dummy;
+        split3(lp - lq, d.ew.d_hi, d.ew.d_lo, dummy);
     }
     if (!kExact) {
-        sw.kind = two_rows ? kResidual : kTargetRow;
-        sw.s = P.s;
-        sw.s0 = P.s0;
+        d.sw.kind = two_rows ? kResidual : kTargetRow;
+        d.sw.s = P.s;
+        d.sw.s0 = P.s0;
     }
-
-    if (k2 == 0) {
-        if (tid == 0) {
-            Selection sel;
-            sel.L = L;
-            sel.bad = bad ? 1 : 0;
-            sel.ew = ew;
-            sel.sw = sw;
-            P.sel[b] = sel;
-        }
-        if (P.tau_out != nullptr && tid < gamma) P.tau_out[(size_t)b * gamma + tid] = tau_s[tid];
-        if (kExact && P.lognorm_out != nullptr)
-            for (int i = tid; i < R; i += kThreads)
-                P.lognorm_out[(size_t)b * R + i] = ((double)rowK[i] + log2(rowS[i])) * 0.693147180559945309417;
-    }
-
-    // this workgroup's chunk of the final distribution
-    const T* rp = target + (size_t)min(L, gamma) * V;
-    const T* rq = draft + (size_t)min(L, gamma - 1) * V;
-    const int begin = k2 * P.chunk2;
-    const int n = min(V, begin + P.chunk2) - begin;
-    float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V + begin : nullptr;
-    double m = 0.0;
-    if (!bad) {
-        if (kExact)
-            m = chunk_weight_sum<D>(rp + begin, rq + begin, n, ew, wrow, scratch);
-        else
-            m = chunk_weight_sum<D>(rp + begin, rq + begin, n, sw, wrow, scratch);
-    }
-    if (tid == 0) P.chunk_mass[(size_t)b * P.nchunk2 + k2] = m;
+    return d;
 }
 
-constexpr int kMaxChunks2 = 1024;
+// b's decision, made once by b's decider workgroup and published as a small
+// record for b's mass and draw workgroups; it also writes the tau / normaliser
+// probes.
+template <class D, bool kExact>
+__device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& sm) {
+    const int gamma = P.gamma, R = 2 * gamma + 1;
+    const int tid = threadIdx.x;
+    const Decision d = decide<D, kExact>(P, b, sm);
+    if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (P.tau_out != nullptr && tid < gamma) P.tau_out[(size_t)b * gamma + tid] = sm.tau[tid];
+    if (kExact && P.lognorm_out != nullptr)
+        for (int i = tid; i < R; i += kThreads)
+            P.lognorm_out[(size_t)b * R + i] = sm.rowL[i] * 0.693147180559945309417;
+    if (tid == 0) {
+        unsigned long long* rec = P.dslot + (size_t)b * kDecisionWords;
+        publish_raw(rec + 1, pack2(d.ew.kp, d.ew.lp_hi));
+        publish_raw(rec + 2, pack2(d.ew.lp_lo, d.ew.kq));
+        publish_raw(rec + 3, pack2(d.ew.lq_hi, d.ew.lq_lo));
+        publish_raw(rec + 4, pack2(d.ew.d_hi, d.ew.d_lo));
+        publish_raw(rec + 0, (unsigned long long)(d.L & 0xffff) | ((unsigned long long)(d.bad ? 1 : 0) << 16) |
+                                 (1ull << 32));
+    }
+}
+
+// b's published decision (in b's mass and draw workgroups).
+__device__ __forceinline__ Decision read_decision(const StepParams& P, int b, bool exact, Smem& sm) {
+    Decision d{};
+    d.ok = wait_raw(P.dslot + (size_t)b * kDecisionWords, kDecisionWords, sm.rec);
+    const unsigned long long w0 = sm.rec[0];
+    d.L = d.ok ? (int)(w0 & 0xffff) : 0;
+    d.bad = ((w0 >> 16) & 1) != 0 || !d.ok;
+    const int kind = (d.L < P.gamma) ? kResidual : kTargetRow;
+    if (exact) {
+        d.ew.kind = kind;
+        d.ew.c = P.c;
+        d.ew.kp = unpack_hi(sm.rec[1]);
+        d.ew.lp_hi = unpack_lo(sm.rec[1]);
+        d.ew.lp_lo = unpack_hi(sm.rec[2]);
+        d.ew.kq = unpack_lo(sm.rec[2]);
+        d.ew.lq_hi = unpack_hi(sm.rec[3]);
+        d.ew.lq_lo = unpack_lo(sm.rec[3]);
+        d.ew.d_hi = unpack_hi(sm.rec[4]);
+        d.ew.d_lo = unpack_lo(sm.rec[4]);
+    } else {
+        d.sw.kind = kind;
+        d.sw.s = P.s;
+        d.sw.s0 = P.s0;
+    }
+    return d;
+}
 
 template <class D, bool kExact>
-__global__ __launch_bounds__(kThreads) void draw_kernel(SelectParams P) {
+__device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Smem& sm) {
     using T = typename D::T;
-    __shared__ double cm[kMaxChunks2];
-    __shared__ double scratch[kWaves];
-    __shared__ double incl_s[kThreads];
-    __shared__ int iscratch[kWaves];
-    __shared__ int fin_chunk;
-    __shared__ double fin_total, fin_t;
-
+    constexpr int E = D::E;
     const int gamma = P.gamma, V = P.V;
-    const int b = blockIdx.x;
-    const int tid = threadIdx.x;
-    const Selection sel = P.sel[b];
-    for (int k = tid; k < P.nchunk2; k += kThreads) cm[k] = P.chunk_mass[(size_t)b * P.nchunk2 + k];
-    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
-    if (sel.bad) {
-        if (tid == 0) {
-            P.accepted_len[b] = -1;
-            P.next_token[b] = -1;
-            if (P.mass_out != nullptr) P.mass_out[b] = __builtin_nan("");
-        }
-        return;
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const Decision d = read_decision(P, b, kExact, sm);
+    if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
+    double m = 0.0;
+    if (!d.ok) {
+        m = __builtin_nan("");
+    } else if (!d.bad && sp.n > 0) {
+        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V + sp.begin;
+        const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V + sp.begin;
+        float* wout = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V + sp.begin : nullptr;
+        m = kExact ? wave_weight_sum<D>(rp, rq, sp.n, d.ew, wout) : wave_weight_sum<D>(rp, rq, sp.n, d.sw, wout);
     }
-    const int L = sel.L;
-    const T* target = static_cast<const T*>(P.target) + (size_t)b * (gamma + 1) * V;
-    const T* draft = static_cast<const T*>(P.draft) + (size_t)b * gamma * V;
-    const T* rp = target + (size_t)min(L, gamma) * V;
-    const T* rq = draft + (size_t)min(L, gamma - 1) * V;
-    ExactWeights ew = sel.ew;
-    SigmoidWeights sw = sel.sw;
-    bool two_rows = L < gamma;
-    float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V : nullptr;
+    if (lane == 0) publish(P.mslot + ((size_t)b * P.nchunk2 + k2) * kWaves + wave, m);
+}
 
-    __syncthreads();
-    if (tid == 0) {
-        double tot = 0.0;
-        for (int k = 0; k < P.nchunk2; ++k) tot += cm[k];
-        fin_total = tot;
-    }
-    __syncthreads();
-    if (two_rows && fin_total == 0.0) {
-        // no residual mass (possible in sigmoid mode): draw from target row L
-        two_rows = false;
-        ew.kind = kTargetRow;
-        sw.kind = kTargetRow;
-        for (int k = 0; k < P.nchunk2; ++k) {
-            const int bk = k * P.chunk2;
-            const int nk = min(V, bk + P.chunk2) - bk;
-            const double mk = kExact ? chunk_weight_sum<D>(rp + bk, rq + bk, nk, ew, wrow ? wrow + bk : nullptr, scratch)
-                                     : chunk_weight_sum<D>(rp + bk, rq + bk, nk, sw, wrow ? wrow + bk : nullptr, scratch);
-            if (tid == 0) cm[k] = mk;
+// The inverse-CDF draw for b, by b's draw workgroup, once b's mass tiles have
+// published.
+template <class D, bool kExact>
+__device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) {
+    using T = typename D::T;
+    constexpr int E = D::E;
+    const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int M = P.nchunk2 * kWaves;
+    Decision d = read_decision(P, b, kExact, sm);
+    unsigned long long* ms = P.mslot + (size_t)b * M;
+    const bool got = d.ok && wait_words(ms, M, sm.sub);
+    if (!got && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
+    const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V;
+    const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V;
+    float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V : nullptr;
+    const int L = d.L;
+    bool bad = d.bad || !got;
+    int idx = -1;
+    double total = __builtin_nan("");
+    for (int pass = 0; pass < 2 && !bad; ++pass) {
+        // fixed-order prefix over the sub-chunk masses: 4 consecutive per thread
+        double loc[4];
+        double ls = 0.0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int j = tid * 4 + i;
+            loc[i] = (j < M) ? sm.sub[j] : 0.0;
+            ls += loc[i];
         }
-        __syncthreads();
-        if (tid == 0) {
-            double tot = 0.0;
-            for (int k = 0; k < P.nchunk2; ++k) tot += cm[k];
-            fin_total = tot;
+        double tot;
+        const double incl = block_inclusive_scan(ls, sm.scratch, &tot);
+        sm.incl[tid] = incl;
+        total = tot;
+        if (!(isfinite(total) && total >= 0.0)) {
+            bad = true;
+            break;
         }
-        __syncthreads();
-    }
-    const double total = fin_total;
-    if (!(isfinite(total) && total > 0.0)) {
-        if (tid == 0) {
-            P.accepted_len[b] = -1;
-            P.next_token[b] = -1;
-            if (P.mass_out != nullptr) P.mass_out[b] = total;
-        }
-        return;
-    }
-    if (tid == 0) {
-        const double t = u * total;
-        double cum = 0.0;
-        int j = -1, lastpos = 0;
-        for (int k = 0; k < P.nchunk2; ++k) {
-            if (cm[k] > 0.0) lastpos = k;
-            if (cum + cm[k] > t) {
-                j = k;
-                break;
+        if (total == 0.0) {
+            if (pass == 0 && L < gamma) {
+                // no residual mass (possible in sigmoid mode): draw from target row L
+                d.ew.kind = kTargetRow;
+                d.sw.kind = kTargetRow;
+                __syncthreads();
+                for (int k2 = 0; k2 < P.nchunk2; ++k2) {
+                    const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
+                    double m = 0.0;
+                    if (sp.n > 0)
+                        m = kExact ? wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, wrow ? wrow + sp.begin : nullptr)
+                                   : wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, wrow ? wrow + sp.begin : nullptr);
+                    if (lane == 0) sm.sub[k2 * kWaves + wave] = m;
+                }
+                __syncthreads();
+                continue;
             }
-            cum += cm[k];
+            bad = true;
+            break;
         }
-        if (j < 0) j = lastpos;  // rounding only
-        fin_chunk = j;
-        fin_t = t - cum;
+        const double t = u * total;
+        const int first = block_first(incl > t, sm.iscratch);
+        if (tid == 0) {
+            sm.cross = -1;
+            sm.cross_t = 0.0;
+        }
+        __syncthreads();
+        if (first < kThreads && tid == first) {
+            double cum = (first == 0) ? 0.0 : sm.incl[first - 1];
+            int j = -1;
+            double before = cum;
+            int lastp = -1;
+            double lastp_before = 0.0;
+            for (int i = 0; i < 4; ++i) {
+                if (loc[i] > 0.0) {
+                    lastp = tid * 4 + i;
+                    lastp_before = cum;
+                }
+                if (j < 0 && cum + loc[i] > t && loc[i] > 0.0) {
+                    j = tid * 4 + i;
+                    before = cum;
+                }
+                cum += loc[i];
+            }
+            if (j < 0) {
+                j = lastp;
+                before = lastp_before;
+            }
+            sm.cross = j;
+            sm.cross_t = t - before;
+        }
+        if (first >= kThreads && tid == 0) {
+            // rounding only: the last positive weight of the last sub-chunk with mass
+            for (int j = M - 1; j >= 0; --j)
+                if (sm.sub[j] > 0.0) {
+                    sm.cross = j;
+                    sm.cross_t = sm.sub[j];
+                    break;
+                }
+        }
+        __syncthreads();
+        const int j = sm.cross;
+        if (j < 0) {
+            bad = true;
+            break;
+        }
+        const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunk2, V, E);
+        const int local = kExact ? sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, sm.cross_t, sm.scratch, sm.incl, sm.iscratch, &sm.result)
+                                 : sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, sm.cross_t, sm.scratch, sm.incl, sm.iscratch, &sm.result);
+        idx = (local >= 0) ? sp.begin + local : -1;
+        if (idx < 0) bad = true;
+        break;
     }
-    __syncthreads();
-    const int j = fin_chunk;
-    const int bj = j * P.chunk2;
-    const int nj = min(V, bj + P.chunk2) - bj;
-    const int idx = kExact ? chunk_find<D>(rp + bj, rq + bj, nj, ew, fin_t, scratch, incl_s, iscratch)
-                           : chunk_find<D>(rp + bj, rq + bj, nj, sw, fin_t, scratch, incl_s, iscratch);
     if (tid == 0) {
-        P.accepted_len[b] = (idx >= 0) ? L : -1;
-        P.next_token[b] = (idx >= 0) ? bj + idx : -1;
-        if (P.mass_out != nullptr) P.mass_out[b] = total;
+        P.accepted_len[b] = bad ? -1 : L;
+        P.next_token[b] = bad ? -1 : idx;
+        if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total;
     }
+    // every workgroup of b is done with b's published words: clear them for the next call
+    __syncthreads();
+    if (kExact)
+        for (int i = tid; i < R * P.nchunk1; i += kThreads) clear_word(P.pslot + (size_t)b * R * P.nchunk1 + i);
+    if (tid < kDecisionWords) clear_word(P.dslot + (size_t)b * kDecisionWords + tid);
+    for (int i = tid; i < M; i += kThreads) clear_word(ms + i);
+}
+
+// Workgroups before block j (see the layout comment of StepParams).
+__device__ __forceinline__ long long block_offset(long long j, long long B, long long S, long long Mt, const int* lag) {
+    auto clampb = [&](long long x) { return x < 0 ? 0 : (x > B ? B : x); };
+    return S * clampb(j) + clampb(j - lag[0]) + Mt * clampb(j - lag[1]) + clampb(j - lag[2]);
+}
+
+template <class D, bool kExact>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void verify_kernel(StepParams P) {
+    __shared__ Smem sm;
+    const long long id = blockIdx.x;
+    const long long B = P.B;
+    const long long S = kExact ? (long long)(2 * P.gamma + 1) * P.nchunk1 : 0;  // stats tiles per element
+    const long long Mt = P.nchunk2;                                            // mass tiles per element
+    // block j holds, in this order: the stats tiles of b = j, the decider of
+    // b = j - lag[0], the mass tiles of b = j - lag[1], the draw of b = j - lag[2]
+    long long lo = 0, hi = B + P.lag[2];  // the block containing id: offset(j) <= id < offset(j + 1)
+    while (hi - lo > 1) {
+        const long long mid = (lo + hi) / 2;
+        if (block_offset(mid, B, S, Mt, P.lag) <= id) lo = mid; else hi = mid;
+    }
+    const long long j = lo;
+    long long r = id - block_offset(j, B, S, Mt, P.lag);
+    if (j < B) {
+        if (r < S) {
+            stats_role<D>(P, (int)(j * S + r), sm);
+            return;
+        }
+        r -= S;
+    }
+    const long long bd = j - P.lag[0];
+    if (bd >= 0 && bd < B) {
+        if (r == 0) {
+            decider_role<D, kExact>(P, (int)bd, sm);
+            return;
+        }
+        r -= 1;
+    }
+    const long long bm = j - P.lag[1];
+    if (bm >= 0 && bm < B) {
+        if (r < Mt) {
+            mass_role<D, kExact>(P, (int)bm, (int)r, sm);
+            return;
+        }
+        r -= Mt;
+    }
+    draw_role<D, kExact>(P, (int)(j - P.lag[2]), sm);
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -689,7 +903,8 @@ struct Plan {
     int E;
     int chunk1, nchunk1;
     int chunk2, nchunk2;
-    size_t off_partial, off_mass, off_sel, bytes;
+    long long n_stats, n_mass, n_total;
+    size_t off_dslot, off_pslot, off_mslot, bytes;
 };
 
 static inline long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
@@ -697,45 +912,64 @@ static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static bool valid_dtype(sv_dtype_t dt) { return dt == SV_F32 || dt == SV_F16 || dt == SV_BF16; }
 
+// Work decomposition; the workspace size depends only on (B, gamma, V, dtype).
 static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* p) {
     if (B < 1 || gamma < 1 || gamma > kMaxGamma || V < 1 || !valid_dtype(dt)) return false;
     const int E = (dt == SV_F32) ? 4 : 8;
     const int s = (dt == SV_F32) ? 4 : 2;
     const long long R = 2LL * gamma + 1;
-    // every row offset is computed in size_t; chunk indices are int
     if ((long long)B * (gamma + 1) * (long long)V > (1LL << 40)) return false;
     const long long min_elems = (long long)kThreads * E;
     const long long max_cells = std::max<long long>(1, ceil_div(V, min_elems));
 
+    // row chunks: enough workgroups to fill the GPU, at most 64 KiB each
     long long nc = ceil_div(kWantStatsTiles, B * R);
     nc = std::max(nc, ceil_div(V, kStatsTileBytes / s));
     nc = std::min(nc, max_cells);
-    long long chunk = ceil_div(ceil_div(V, nc), E) * E;
+    nc = std::min(nc, std::max<long long>(1, kMergeCap / R));
+    const long long chunk = ceil_div(ceil_div(V, nc), E) * E;
     p->chunk1 = (int)chunk;
     p->nchunk1 = (int)ceil_div(V, chunk);
-    if ((long long)B * R * p->nchunk1 > 0x7fffffffLL) return false;
+    if (R * p->nchunk1 > kMergeCap) return false;
 
-    const long long max_scan = (long long)kScanVec * kThreads * E;  // in-chunk scan capacity
+    // final-distribution tiles: a sub-chunk (a quarter tile) must fit one
+    // vector per thread, and b's sub-chunk masses must fit kMaxSub
+    const long long max_tile_vecs = (long long)kWaves * kThreads;
     long long nc2 = ceil_div(kWantSampleTiles, B);
     nc2 = std::max(nc2, ceil_div(V, kSampleTileBytes / s));
     nc2 = std::min(nc2, max_cells);
-    nc2 = std::max(nc2, ceil_div(V, max_scan));
-    long long chunk2 = ceil_div(ceil_div(V, nc2), E) * E;
+    nc2 = std::max(nc2, ceil_div(V, max_tile_vecs * E));
+    const long long chunk2 = ceil_div(ceil_div(V, nc2), E) * E;
     p->chunk2 = (int)chunk2;
     p->nchunk2 = (int)ceil_div(V, chunk2);
-    if ((long long)B * p->nchunk2 > 0x7fffffffLL) return false;
+    if ((long long)p->nchunk2 * kWaves > kMaxSub || chunk2 / E > max_tile_vecs) return false;
     p->E = E;
 
-    if (p->nchunk2 > kMaxChunks2) return false;
-    size_t off = 0;
-    p->off_sel = off;
-    off = align256(off + sizeof(Selection) * (size_t)B);
-    p->off_mass = off;
-    off = align256(off + sizeof(double) * (size_t)B * p->nchunk2);
-    p->off_partial = off;
-    off = align256(off + sizeof(RowPartial) * (size_t)B * R * p->nchunk1);
+    p->n_stats = (long long)B * R * p->nchunk1;
+    p->n_mass = (long long)B * p->nchunk2;
+    p->n_total = p->n_stats + p->n_mass + 2LL * B;  // plus a decider and a draw per batch element
+    if (p->n_total > 0x7fffffffLL) return false;
+
+    size_t off = 256;  // header: the error flag at byte offset 4
+    p->off_dslot = off;
+    off = align256(off + sizeof(unsigned long long) * (size_t)B * kDecisionWords);
+    p->off_pslot = off;
+    off = align256(off + sizeof(unsigned long long) * (size_t)p->n_stats);
+    p->off_mslot = off;
+    off = align256(off + sizeof(unsigned long long) * (size_t)p->n_mass * kWaves);
     p->bytes = off;
     return true;
+}
+
+// Block lags (in batch elements) of the decider, mass and draw roles.  The
+// decider of b follows b's stats tiles at once; mass and draw workgroups come
+// after the whole stream: interleaving them into it was measured to cost more
+// (their latency-bound lifetimes hold dispatch slots the stream needs) than
+// the overlap gains.
+static void set_lags(long long B, int* lag) {
+    lag[0] = 1;
+    lag[1] = (int)B;
+    lag[2] = (int)B + 1;
 }
 
 struct Call {
@@ -759,13 +993,8 @@ struct Call {
 
 template <class D>
 static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
-    using T = typename D::T;
-    const T* draft = static_cast<const T*>(a.draft);
-    const T* target = static_cast<const T*>(a.target);
     char* ws = static_cast<char*>(a.ws);
-    RowPartial* partial = reinterpret_cast<RowPartial*>(ws + pl.off_partial);
-
-    SelectParams P{};
+    StepParams P{};
     P.draft = a.draft;
     P.target = a.target;
     P.tokens = a.tokens;
@@ -773,35 +1002,34 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.B = a.B;
     P.gamma = a.gamma;
     P.V = a.V;
+    P.chunk1 = pl.chunk1;
     P.nchunk1 = pl.nchunk1;
     P.chunk2 = pl.chunk2;
     P.nchunk2 = pl.nchunk2;
+    P.n_stats = exact ? (int)pl.n_stats : 0;
+    P.n_mass = (int)pl.n_mass;
+    P.n_total = P.n_stats + P.n_mass + 2 * a.B;
+    set_lags(a.B, P.lag);
     P.temperature = (double)a.temperature;
     P.alpha = (double)a.alpha;
     P.beta = (double)a.beta;
     P.c = (float)(1.4426950408889634074 / (double)a.temperature);
     P.s = (float)(1.0 / ((double)a.temperature * ((double)a.beta - (double)a.alpha)));
     P.s0 = (float)(-(double)a.alpha / ((double)a.beta - (double)a.alpha));
-    P.partial = partial;
-    P.chunk_mass = reinterpret_cast<double*>(ws + pl.off_mass);
-    P.sel = reinterpret_cast<Selection*>(ws + pl.off_sel);
+    P.error = reinterpret_cast<unsigned int*>(ws) + 1;
+    P.dslot = reinterpret_cast<unsigned long long*>(ws + pl.off_dslot);
+    P.pslot = reinterpret_cast<unsigned long long*>(ws + pl.off_pslot);
+    P.mslot = reinterpret_cast<unsigned long long*>(ws + pl.off_mslot);
     P.accepted_len = a.accepted_len;
     P.next_token = a.next_token;
     P.tau_out = a.tau_out;
     P.weight_out = a.weight_out;
     P.mass_out = a.mass_out;
     P.lognorm_out = a.lognorm_out;
-
-    if (exact) {
-        const int tiles = a.B * (2 * a.gamma + 1) * pl.nchunk1;
-        hipLaunchKernelGGL(row_stats_kernel<D>, dim3(tiles), dim3(kThreads), 0, a.stream, draft, target, a.gamma,
-                           a.V, pl.chunk1, pl.nchunk1, P.c, partial);
-        hipLaunchKernelGGL((mass_kernel<D, true>), dim3(a.B * pl.nchunk2), dim3(kThreads), 0, a.stream, P);
-        hipLaunchKernelGGL((draw_kernel<D, true>), dim3(a.B), dim3(kThreads), 0, a.stream, P);
-    } else {
-        hipLaunchKernelGGL((mass_kernel<D, false>), dim3(a.B * pl.nchunk2), dim3(kThreads), 0, a.stream, P);
-        hipLaunchKernelGGL((draw_kernel<D, false>), dim3(a.B), dim3(kThreads), 0, a.stream, P);
-    }
+    if (exact)
+        hipLaunchKernelGGL((verify_kernel<D, true>), dim3(P.n_total), dim3(kThreads), 0, a.stream, P);
+    else
+        hipLaunchKernelGGL((verify_kernel<D, false>), dim3(P.n_total), dim3(kThreads), 0, a.stream, P);
     return hipGetLastError() == hipSuccess ? SV_OK : SV_ERR_HIP;
 }
 

@@ -23,13 +23,6 @@ constexpr int kUnroll = 8;               // 16-byte loads in flight per thread
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
-// One chunk's contribution to a row normaliser: sum_x 2^(w(x) log2e - k) = s.
-struct RowPartial {
-    double s;
-    float k;
-    float pad;
-};
-
 // ---------------------------------------------------------------------------
 // storage types: E elements per 16-byte vector
 // ---------------------------------------------------------------------------

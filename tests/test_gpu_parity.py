@@ -193,6 +193,21 @@ def test_deterministic_and_workspace_reuse():
     assert binding.workspace_bytes(3, 2, 999, torch.bfloat16) <= ws.numel()
     compare(small, run_gpu(small, workspace=ws), run_oracle(small), label="reuse smaller")
     compare(big, run_gpu(big, workspace=ws), run_oracle(big), label="reuse bigger again")
+    # every call hands the workspace back zero-filled: ticket counter reset,
+    # published words cleared, no timed-out wait
+    torch.cuda.synchronize()
+    assert int(torch.count_nonzero(ws)) == 0
+
+
+@pytest.mark.parametrize("mode", ["exact", "sigmoid"])
+def test_workspace_returns_to_zero(mode):
+    x = W.small_case(5, 4, 7001, "f16", mode=mode, seed=81, alpha=-1e3, beta=1e3)
+    x.tokens[1, 0] = -1                        # a sentinel row must clean up too
+    ws = binding.new_workspace(5, 4, 7001, torch.float16, "cuda")
+    for _ in range(3):
+        run_gpu(x, workspace=ws)
+        torch.cuda.synchronize()
+        assert int(torch.count_nonzero(ws)) == 0
 
 
 def test_gpu_emits_target_distribution_tiny_vocab():
