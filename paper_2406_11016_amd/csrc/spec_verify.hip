@@ -175,7 +175,11 @@ __device__ __forceinline__ void load_pair_u(const typename D::T* rp, const typen
 }
 
 constexpr int kPassUnroll = 4;  // vectors in flight per lane in the weight pass
-constexpr int kMergeCap = 1024;  // chunk log-normalisers of one batch element (2 gamma + 1 rows)
+constexpr int kMaxStatsSub = kWaves * kMaxRows;  // stats sub-chunks of one batch element (2 gamma + 1 rows)
+// Per batch element the stats words hold 2 gamma + 1 rows x nchunk1 x kWaves
+// (K, S) pairs, then one more pair: the token drawn from target row gamma and
+// the draw's total mass (see bonus_role).
+constexpr int kFindVec = 4;      // vectors per thread when the decider scans a stats sub-chunk
 constexpr int kMaxSub = 1024;    // sub-chunk masses of one batch element (nchunk2 * kWaves)
 constexpr int kMaxSpins = 1 << 17;  // bound on every wait (about 0.1 s), so every wave exits
 constexpr int kDecisionWords = 5;          // L and the sentinel flag, then 8 floats of weight constants
@@ -214,16 +218,32 @@ __device__ __forceinline__ unsigned long long pack2(float a, float b) {
 __device__ __forceinline__ float unpack_hi(unsigned long long w) { return __uint_as_float((unsigned int)(w >> 32)); }
 __device__ __forceinline__ float unpack_lo(unsigned long long w) { return __uint_as_float((unsigned int)w); }
 
-// Waits until the n raw words at p are published and copies them to dst.
-__device__ __forceinline__ bool wait_raw(unsigned long long* p, int n, unsigned long long* dst) {
+// Waits until the n words at p are published, handing each to take(i, w)
+// (w the raw, still inverted word).  Called by every thread; returns false
+// after kMaxSpins polls.  Each poll issues NV loads per thread before it
+// looks at any (indices clamped into range), so a poll costs one memory
+// round trip for up to NV * kThreads words.
+template <int NV, class F>
+__device__ __forceinline__ bool poll_words(unsigned long long* p, int n, F take) {
     for (int spin = 0;; ++spin) {
         int missing = 0;
-        for (int i = threadIdx.x; i < n; i += kThreads) {
-            const unsigned long long w = __hip_atomic_load(p + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (w == 0ull)
-                missing = 1;
-            else
-                dst[i] = ~w;
+        for (int i0 = 0; i0 < n; i0 += NV * kThreads) {
+            unsigned long long w[NV];
+#pragma unroll
+            for (int u = 0; u < NV; ++u) {
+                const int i = min(i0 + u * kThreads + (int)threadIdx.x, n - 1);
+                w[u] = __hip_atomic_load(p + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+#pragma unroll
+            for (int u = 0; u < NV; ++u) {
+                const int i = i0 + u * kThreads + (int)threadIdx.x;
+                if (i < n) {
+                    if (w[u] == 0ull)
+                        missing = 1;
+                    else
+                        take(i, w[u]);
+                }
+            }
         }
         if (__syncthreads_or(missing) == 0) return true;
         if (spin >= kMaxSpins) return false;
@@ -231,22 +251,24 @@ __device__ __forceinline__ bool wait_raw(unsigned long long* p, int n, unsigned 
     }
 }
 
-// Waits until the n words at p are published and copies them, decoded, to
-// dst (LDS).  Called by every thread; returns false after kMaxSpins polls.
+// The n (<= kThreads) raw record words at p, copied to dst.
+__device__ __forceinline__ bool wait_raw(unsigned long long* p, int n, unsigned long long* dst) {
+    return poll_words<1>(p, n, [&](int i, unsigned long long w) { dst[i] = ~w; });
+}
+
+// The n words at p, decoded to dst (LDS).
 __device__ __forceinline__ bool wait_words(unsigned long long* p, int n, double* dst) {
-    for (int spin = 0;; ++spin) {
-        int missing = 0;
-        for (int i = threadIdx.x; i < n; i += kThreads) {
-            const unsigned long long w = __hip_atomic_load(p + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (w == 0ull)
-                missing = 1;
-            else
-                dst[i] = decode_word(w);
-        }
-        if (__syncthreads_or(missing) == 0) return true;
-        if (spin >= kMaxSpins) return false;
-        __builtin_amdgcn_s_sleep(2);
-    }
+    return poll_words<4>(p, n, [&](int i, unsigned long long w) { dst[i] = decode_word(w); });
+}
+
+// The n (K, S) word pairs at p, decoded to K[i] (float) and S[i] (LDS).
+__device__ __forceinline__ bool wait_ks(unsigned long long* p, int n, float* K, double* S) {
+    return poll_words<4>(p, 2 * n, [&](int i, unsigned long long w) {
+        if (i & 1)
+            S[i >> 1] = decode_word(w);
+        else
+            K[i >> 1] = (float)decode_word(w);
+    });
 }
 
 // ---------------------------------------------------------------------------
@@ -338,25 +360,29 @@ __device__ __forceinline__ int block_first(bool pred, int* iscratch /* [kWaves] 
 
 // Index (relative to the sub-chunk start) of the first element whose running
 // weight sum exceeds t, or of the last positive weight if rounding leaves the
-// sub-chunk total at or below t.  Thread i holds vector i (n <= kThreads * E),
-// so one workgroup scan follows element order.  Valid in every thread.
-template <class D, int KIND, class W>
+// sub-chunk total at or below t.  Thread i holds vectors i NV .. i NV + NV - 1
+// (n <= kThreads * NV * E), so one workgroup scan follows element order.
+// Valid in every thread.
+template <class D, int KIND, int NV, class W>
 __device__ __forceinline__ int sub_chunk_find_k(const typename D::T* rp, const typename D::T* rq, int n,
                                                 const W& w, double t, double* scratch, double* incl_s,
                                                 int* iscratch, int* result) {
     constexpr int E = D::E;
+    constexpr int NE = NV * E;
     constexpr bool two_rows = (KIND == kResidual);
     const int tid = threadIdx.x;
     const bool fast = pair_aligned<D>(rp, rq, two_rows);
-    float zp[1][E], zq[1][E];
-    load_pair_u<D, 1>(rp, rq, two_rows, fast, tid, 1, n, zp, zq);
-    float a[E];
+    float zp[NV][E], zq[NV][E];
+    load_pair_u<D, NV>(rp, rq, two_rows, fast, tid * NV, 1, n, zp, zq);
+    float a[NE];
     double sum = 0.0;
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-        a[e] = w.template eval<KIND>(zp[0][e], zq[0][e]);
-        sum += (double)a[e];
-    }
+    for (int u = 0; u < NV; ++u)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            a[u * E + e] = w.template eval<KIND>(zp[u][e], zq[u][e]);
+            sum += (double)a[u * E + e];
+        }
     if (tid == 0) *result = -1;
     double tot;
     const double incl = block_inclusive_scan(sum, scratch, &tot);
@@ -367,20 +393,20 @@ __device__ __forceinline__ int sub_chunk_find_k(const typename D::T* rp, const t
             double cum = (first == 0) ? 0.0 : incl_s[first - 1];
             int idx = -1, lastp = -1;
 #pragma unroll
-            for (int e = 0; e < E; ++e) {
+            for (int e = 0; e < NE; ++e) {
                 if (a[e] > 0.0f) lastp = e;
                 cum += (double)a[e];
                 if (idx < 0 && cum > t && a[e] > 0.0f) idx = e;
             }
             if (idx < 0) idx = lastp;
-            *result = (idx >= 0) ? tid * E + idx : -1;
+            *result = (idx >= 0) ? tid * NE + idx : -1;
         }
     } else {
         // t lies at or beyond the sub-chunk total (rounding only): the last positive weight
         int lastp = -1;
 #pragma unroll
-        for (int e = 0; e < E; ++e)
-            if (a[e] > 0.0f) lastp = tid * E + e;
+        for (int e = 0; e < NE; ++e)
+            if (a[e] > 0.0f) lastp = tid * NE + e;
         const int lv = wave_max_int(lastp);
         if ((tid % kWave) == 0) iscratch[tid / kWave] = lv;
         __syncthreads();
@@ -397,48 +423,73 @@ __device__ __forceinline__ int sub_chunk_find_k(const typename D::T* rp, const t
 template <class D, class W>
 __device__ int sub_chunk_find(const typename D::T* rp, const typename D::T* rq, int n, const W& w, double t,
                               double* scratch, double* incl_s, int* iscratch, int* result) {
-    return (w.kind == kTargetRow) ? sub_chunk_find_k<D, kTargetRow>(rp, rq, n, w, t, scratch, incl_s, iscratch, result)
-                                  : sub_chunk_find_k<D, kResidual>(rp, rq, n, w, t, scratch, incl_s, iscratch, result);
+    return (w.kind == kTargetRow) ? sub_chunk_find_k<D, kTargetRow, 1>(rp, rq, n, w, t, scratch, incl_s, iscratch, result)
+                                  : sub_chunk_find_k<D, kResidual, 1>(rp, rq, n, w, t, scratch, incl_s, iscratch, result);
 }
 
 // ---------------------------------------------------------------------------
 // the fused step: one launch; a workgroup's role follows from its index
-//   stats (b, r, k)  exact mode: chunk k of row r of batch element b -> the
-//                    chunk's log-normaliser (eq. (4)), published
+//   stats (b, r, k)  exact mode: chunk k of row r of batch element b; each
+//                    wave publishes its contiguous quarter's normaliser
+//                    terms (eq. (4)) as a (K, S) pair
 //   decider (b)      b's decision -- eq. (1) at the drafted tokens and the
-//                    first-rejection scan -- published as a small record
+//                    first-rejection scan -- published as a small record;
+//                    when every draft is accepted it also draws the next
+//                    token from target row gamma itself (see decider_role)
 //   mass (b, k2)     the masses of the final distribution (eqs. (2)-(3) or
 //                    the bonus row) over tile k2, one per wave, published
 //   draw (b)         the inverse-CDF draw of b's next token; clears b's
 //                    published words for the next call
-// Index order runs over blocks j = 0, 1, ...; block j holds the stats tiles
-// of b = j, the decider of b = j - lag[0], the mass tiles of b = j - lag[1]
-// and the draw of b = j - lag[2], so each role of b comes after the roles it
-// reads and the lags let the stream of later batch elements cover the
-// latency of earlier ones.  A workgroup only waits on results of workgroups
-// with smaller indices, and never on a returning atomic: the streaming
-// workgroups publish and retire.  Each XCD dispatches its workgroups in index
-// order, so the waiting workgroup with the smallest index always waits on
-// workgroups that are running and do not wait, or that its XCD will dispatch
-// once its running, non-waiting workgroups finish: no wait can block forever.
-// Every wait is also bounded (kMaxSpins), so every wave exits regardless.
+// Index order: first the stats tiles of target row gamma of every batch
+// element and then a bonus workgroup per element (exact mode), then units
+// u = 0, 1, ...: unit u holds the stats
+// tiles of the other rows and then the decider of b = u (for u < B),
+// followed by the mass tiles and then the draw of b = u - lagM (for
+// u >= lagM).  So each role of b comes
+// after the roles it reads, and lagM lets the stream of later batch elements
+// cover the latency of earlier ones.  A workgroup only waits on results of
+// workgroups with smaller indices, and never on a returning atomic: the
+// streaming workgroups publish and retire.  Each XCD dispatches its
+// workgroups in index order, so the waiting workgroup with the smallest index
+// always waits on workgroups that are running and do not wait, or that its
+// XCD will dispatch once its running, non-waiting workgroups finish: no wait
+// can block forever.  Every wait is also bounded (kMaxSpins), so every wave
+// exits regardless.
+//
+// Units fall into three segments of uniform unit size (stats + decider;
+// all four roles; mass + draw), so a workgroup finds its role with one
+// division, from kernel arguments that sit in the first cache lines of the
+// argument block together with everything the stats role reads: a stats
+// workgroup starts its stream after a single argument fetch.
 // ---------------------------------------------------------------------------
+struct Layout {
+    unsigned int endg;                 // stats tiles of the target rows gamma (B nchunk1, or 0)
+    unsigned int endd;                 // ... then one bonus workgroup per batch element (or none)
+    unsigned int end0, end1;           // first workgroup index of segments 1 and 2, counted after endg
+    unsigned int size0, size1, size2;  // workgroups per unit in segments 0, 1, 2
+    int lagM;                          // unit lag of the mass and draw roles
+    int b2;                            // batch element of the first unit of segment 2
+    int S;                             // stats tiles per unit: rows other than gamma (0 in sigmoid mode)
+    int Mt;                            // mass tiles per batch element
+};
+
 struct StepParams {
+    Layout y;
     const void* draft;
     const void* target;
-    const int32_t* tokens;
-    const float* uniforms;
+    unsigned long long* pslot;     // [B, (2 gamma + 1) nchunk1 kWaves + 1, 2] stats (K, S) pairs, bonus draw
     int B, gamma, V;
     int chunk1, nchunk1;           // exact: row chunks
-    int chunk2, nchunk2;           // final-distribution tiles per batch element
-    int n_stats, n_mass, n_total;  // workgroups by role
-    int lag[3];                    // block lags of the decider, mass and draw roles
     float c;                       // exact: log2(e) / T
+    int chunk2, nchunk2;           // final-distribution tiles per batch element
     float s, s0;                   // sigmoid: u = fma(z, s, s0)
+    int bonus_direct;              // exact: b's bonus workgroup draws from target row gamma (see bonus_role)
+    int pstride;                   // stats words per batch element
+    const int32_t* tokens;
+    const float* uniforms;
     double temperature, alpha, beta;
     unsigned int* error;           // set to 1 if a wait ever timed out
-    unsigned long long* dslot;     // [B, kDecisionWords] the published decision (exact mode)
-    unsigned long long* pslot;     // [B, 2 gamma + 1, nchunk1] chunk log2-normalisers
+    unsigned long long* dslot;     // [B, nchunk2 + 1, kDecisionWords] copies of the published decision
     unsigned long long* mslot;     // [B, nchunk2, kWaves] sub-chunk masses
     int32_t* accepted_len;
     int32_t* next_token;
@@ -449,10 +500,11 @@ struct StepParams {
 };
 
 struct Smem {
-    double words[kMergeCap];   // exact: b's chunk log2-normalisers
+    float K[kMaxStatsSub + 1];   // exact: b's stats sub-chunk references
+    double S[kMaxStatsSub + 1];  //        and sums (then the bonus draw's token and total)
     double rowL[kMaxRows];     // exact: b's row log2-normalisers
+    float rowK[kMaxRows];      //        and the largest reference of each row
     double tau[kMaxGamma];
-    int stop[kMaxGamma];
     double sub[kMaxSub];       // draw: b's sub-chunk masses
     double incl[kThreads];
     double scratch[kWaves];
@@ -460,7 +512,9 @@ struct Smem {
     float sk[kWaves];
     double ss[kWaves];
     unsigned long long rec[kDecisionWords];
-    int L, bad, tok_bad, timed_out, result, cross, last;
+    int result, cross;
+    float kmax;
+    unsigned long long flags[kWaves][3];
     double cross_t;
 };
 
@@ -472,60 +526,149 @@ __device__ __forceinline__ void split3(double v, float& hi, float& mid, float& l
     lo = (float)((v - (double)hi) - (double)mid);
 }
 
-// Exact mode, one chunk of one row: sum_x 2^(z c - k) in one streaming pass,
-// published as the chunk's log2-normaliser k + log2(s).
+// Exact mode, one chunk of one row: sum_x 2^(z c - K) in one streaming pass.
+// Wave w covers the contiguous quarter sub_chunk(k, w, ...) of the chunk and
+// publishes its pair (K, S): K an integral reference (or -inf), S the fp64 sum
+// of 2^(z c - K) over its elements, so sum_x e^(z/T) = sum over quarters of
+// S 2^K, merged later by exact power-of-two scaling.
 template <class D>
-__device__ __forceinline__ void stats_role(const StepParams& P, int tile, Smem& sm) {
+__device__ __forceinline__ void stats_role(const StepParams& P, int b, int r, int k) {
     using T = typename D::T;
     constexpr int E = D::E;
-    const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1, nchunk = P.nchunk1, chunk = P.chunk1;
+    const int gamma = P.gamma, V = P.V;
     const float c = P.c;
-    const int k = tile % nchunk;
-    const int rowid = tile / nchunk;  // b * R + r
-    const int b = rowid / R;
-    const int r = rowid - b * R;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const T* row = (r <= gamma) ? static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + r) * (size_t)V
                                 : static_cast<const T*>(P.draft) + ((size_t)b * gamma + (r - gamma - 1)) * (size_t)V;
-    const int begin = k * chunk;
-    const int n = min(V, begin + chunk) - begin;
-    const T* base = row + begin;
-    const int nfull = n / E;            // whole 16-byte vectors
-    const int nvec = (n + E - 1) / E;   // plus a partial one at the end of a row
+    const Span sp = sub_chunk(k, wave, P.chunk1, V, E);
+    const T* base = row + sp.begin;
+    const int n = sp.n;
+    const int nfull = n / E;  // whole 16-byte vectors
     const bool aligned = (reinterpret_cast<uintptr_t>(base) & 15u) == 0;
 
-    // Thread t takes whole vectors t, t + kThreads, ... in blocks of kUnroll;
-    // all loads of a block are issued before any is used, and the block shares
-    // one update of the running reference.  A partial vector at the end of a
-    // row is absorbed after the loop by the thread that would own it.  The
-    // assignment and order depend only on element indices, never on the
-    // row's address, so equal rows give bit-identical normalisers.
+    // Lane l takes whole vectors l, l + 64, ... of the quarter in blocks of
+    // kUnroll; all loads of a block are issued before any is used, and the
+    // block shares one update of the running reference.  A partial vector at
+    // the end of a row is absorbed after the loop.  The assignment and order
+    // depend only on element indices, never on the row's address, so equal
+    // rows give bit-identical sums.
     Lse st{-INFINITY, 0.0};
-    if (nfull > 0) {
-        for (int v0 = 0; v0 < nfull; v0 += kUnroll * kThreads) {
-            float x[kUnroll][E];
-            if (aligned) {
-                u32x4 raw[kUnroll];
+    for (int v0 = 0; v0 < nfull; v0 += kUnroll * kWave) {
+        float x[kUnroll][E];
+        if (aligned) {
+            u32x4 raw[kUnroll];
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u)
-                    raw[u] = load_vec_or_pad<D, true>(base, v0 + u * kThreads + (int)threadIdx.x, nfull);
+            for (int u = 0; u < kUnroll; ++u) raw[u] = load_vec_or_pad<D, true>(base, v0 + u * kWave + lane, nfull);
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) unpack<D>(raw[u], x[u]);
-            } else {
-                // rows that are not 16-byte aligned (e.g. odd V in fp32)
+            for (int u = 0; u < kUnroll; ++u) unpack<D>(raw[u], x[u]);
+        } else {
+            // rows that are not 16-byte aligned (e.g. odd V in fp32)
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u)
-                    load_elems_or_pad<D>(base, (v0 + u * kThreads + (int)threadIdx.x) * E, nfull * E, x[u]);
-            }
-            lse_absorb_block<kUnroll, E>(st, x, c);
+            for (int u = 0; u < kUnroll; ++u)
+                load_elems_or_pad<D>(base, (v0 + u * kWave + lane) * E, nfull * E, x[u]);
         }
+        lse_absorb_block<kUnroll, E>(st, x, c);
     }
-    if (nvec > nfull && (int)threadIdx.x == nfull % kThreads) {
+    if (n > nfull * E && lane == nfull % kWave) {
         float x[1][E];
         load_elems_or_pad<D>(base, nfull * E, n, x[0]);
         lse_absorb_block<1, E>(st, x, c);
     }
-    const Lse blk = block_lse(st, sm.sk, sm.ss);
-    if (threadIdx.x == 0) publish(P.pslot + tile, (double)blk.k + log2(blk.s));
+    const Lse w = wave_lse(st);
+    if (lane == 0) {
+        const size_t sub = ((size_t)r * P.nchunk1 + k) * kWaves + wave;
+        unsigned long long* out = P.pslot + (size_t)b * P.pstride + sub * 2;
+        publish(out, (double)w.k);
+        publish(out + 1, w.s);
+    }
+}
+
+// Row log2-normalisers Lambda = Kmax + log2(sum S 2^(K - Kmax)) of R rows
+// from the (K, S) pairs of their W sub-chunks in LDS, into sm.rowL / sm.rowK:
+// one thread per row, in sub-chunk order, reading blocks of 16 pairs at a time
+// (clamped, masked indices) so each block costs one LDS round trip.  Ends
+// with a workgroup barrier.
+__device__ __forceinline__ void merge_rows(Smem& sm, int R, int W) {
+    constexpr int U = 16;
+    for (int i = threadIdx.x; i < R; i += kThreads) {
+        const float* K = sm.K + (size_t)i * W;
+        const double* S = sm.S + (size_t)i * W;
+        float m = -INFINITY;
+        for (int j0 = 0; j0 < W; j0 += U) {
+            float k[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) k[u] = K[min(j0 + u, W - 1)];
+#pragma unroll
+            for (int u = 0; u < U; ++u) m = fmaxf(m, k[u]);  // repeats of the last pair change nothing
+        }
+        double sum = 0.0;
+        for (int j0 = 0; j0 < W; j0 += U) {
+            float k[U];
+            double t[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                k[u] = K[min(j0 + u, W - 1)];
+                t[u] = S[min(j0 + u, W - 1)];
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (j0 + u < W) sum += ldexp(t[u], exp_delta(k[u] - m));
+        }
+        // a NaN logit makes S NaN; a +inf logit makes K +inf and S NaN
+        sm.rowL[i] = (sum != sum) ? __builtin_nan("") : ((m == -INFINITY) ? -INFINITY : (double)m + log2(sum));
+        sm.rowK[i] = m;
+    }
+    __syncthreads();
+}
+
+// For the drafts c < gamma (thread c holds stop_c: 0 accepted, 1 rejected, 2
+// unreadable, and tok_ok): the first c with stop_c != 0 (kThreads if none),
+// whether that one is unreadable, and whether any drafted token is out of
+// range.  One workgroup barrier.
+__device__ __forceinline__ void scan_stops(int stop, bool tok_ok, Smem& sm, int* first, bool* first_bad,
+                                           bool* tok_bad) {
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const unsigned long long rej = __ballot(stop != 0);
+    const unsigned long long unr = __ballot(stop == 2);
+    const unsigned long long tok = __ballot(!tok_ok);
+    if (lane == 0) {
+        sm.flags[wave][0] = rej;
+        sm.flags[wave][1] = unr;
+        sm.flags[wave][2] = tok;
+    }
+    __syncthreads();
+    int f = kThreads;
+    bool fb = false, tb = false;
+#pragma unroll
+    for (int w = kWaves - 1; w >= 0; --w) {
+        const unsigned long long r = sm.flags[w][0];
+        if (r != 0) {
+            const int l = __ffsll((long long)r) - 1;
+            f = w * kWave + l;
+            fb = ((sm.flags[w][1] >> l) & 1ull) != 0;
+        }
+        tb |= sm.flags[w][2] != 0;
+    }
+    *first = f;
+    *first_bad = fb;
+    *tok_bad = tb;
+}
+
+// The largest of one row's W sub-chunk references (valid in every thread).
+__device__ __forceinline__ float row_kmax(Smem& sm, const float* K, int W) {
+    const int tid = threadIdx.x;
+    float m = -INFINITY;
+    for (int j = tid; j < W; j += kThreads) m = fmaxf(m, K[j]);
+    m = wave_max(m);
+    if (tid % kWave == 0) sm.sk[tid / kWave] = m;
+    __syncthreads();
+    if (tid == 0) {
+        float mm = sm.sk[0];
+        for (int w = 1; w < kWaves; ++w) mm = fmaxf(mm, sm.sk[w]);
+        sm.kmax = mm;
+    }
+    __syncthreads();
+    return sm.kmax;
 }
 
 struct Decision {
@@ -552,7 +695,6 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     double r = 0.0;
     bool tok_ok = true;
     float zp = 0.0f, zq = 0.0f;
-    if (tid == 0) sm.tok_bad = 0;
     if (tid < gamma) {
         x = P.tokens[(size_t)b * gamma + tid];
         r = (double)P.uniforms[(size_t)b * (gamma + 1) + tid];
@@ -565,27 +707,16 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     Decision d{};
     d.ok = true;
     if (kExact) {
-        // b's chunk log2-normalisers, then each row's, merged in chunk order
-        const int nc1 = P.nchunk1;
-        d.ok = wait_words(P.pslot + (size_t)b * R * nc1, R * nc1, sm.words);
-        for (int i = tid; i < R; i += kThreads) {
-            double m = -INFINITY;
-            bool nan = false;
-            for (int k = 0; k < nc1; ++k) {
-                const double l = sm.words[i * nc1 + k];
-                nan |= (l != l);
-                m = fmax(m, l);
-            }
-            double sum = 0.0;
-            if (!nan && m != -INFINITY)
-                for (int k = 0; k < nc1; ++k) sum += exp2(sm.words[i * nc1 + k] - m);
-            sm.rowL[i] = nan ? __builtin_nan("") : ((m == -INFINITY) ? -INFINITY : m + log2(sum));
-        }
+        // b's stats sub-chunk pairs (K, S), then each row's log2-normaliser
+        // max K + log2(sum S 2^(K - max K)), merged in sub-chunk order by
+        // exact power-of-two scaling
+        const int W = kWaves * P.nchunk1;  // sub-chunks per row
+        d.ok = wait_ks(P.pslot + (size_t)b * P.pstride, R * W + (P.bonus_direct ? 1 : 0), sm.K, sm.S);
+        merge_rows(sm, R, W);
     }
-    __syncthreads();
 
+    int stop = 0;
     if (tid < gamma) {
-        if (!tok_ok) sm.tok_bad = 1;
         double tau;
         bool row_ok;
         if (kExact) {
@@ -608,25 +739,14 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
             row_ok = isfinite(tau);
         }
         sm.tau[tid] = tau;
-        sm.stop[tid] = !row_ok ? 2 : ((r <= tau) ? 0 : 1);
+        stop = !row_ok ? 2 : ((r <= tau) ? 0 : 1);
     }
-    __syncthreads();
-    if (tid == 0) {
-        int L = gamma, bad = sm.tok_bad;
-        for (int c = 0; c < gamma; ++c) {
-            if (sm.stop[c] != 0) {
-                L = c;
-                if (sm.stop[c] == 2) bad = 1;
-                break;
-            }
-        }
-        if (kExact && !bad && L == gamma && !isfinite(sm.rowL[gamma])) bad = 1;
-        sm.L = L;
-        sm.bad = bad;
-    }
-    __syncthreads();
-    d.L = sm.L;
-    d.bad = sm.bad != 0 || !d.ok;
+    // the first draft that is rejected (or unreadable) ends the accepted prefix
+    int first;
+    bool first_bad, tok_bad;
+    scan_stops(stop, tok_ok, sm, &first, &first_bad, &tok_bad);
+    d.L = min(first, gamma);
+    d.bad = tok_bad || first_bad || !d.ok || (kExact && d.L == gamma && !isfinite(sm.rowL[gamma]));
     const bool two_rows = d.L < gamma;
     if (kExact && !d.bad) {
         const double lp = sm.rowL[min(d.L, gamma)];
@@ -646,34 +766,190 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     return d;
 }
 
+// Fixed-order prefix over M (<= 4 kThreads) masses m[] in LDS, four
+// consecutive ones per thread: loc receives the thread's masses, sm.incl[tid]
+// its inclusive prefix.  Returns the total, valid in every thread.
+__device__ __forceinline__ double mass_prefix(const double* m, int M, Smem& sm, double (&loc)[4]) {
+    const int tid = threadIdx.x;
+    double ls = 0.0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int j = tid * 4 + i;
+        loc[i] = (j < M) ? m[j] : 0.0;
+        ls += loc[i];
+    }
+    double tot;
+    sm.incl[tid] = block_inclusive_scan(ls, sm.scratch, &tot);
+    return tot;
+}
+
+// After mass_prefix: the index of the mass in which the running sum first
+// exceeds t (or the last positive one, if rounding leaves the total at or
+// below t), with t minus the running sum before it in *t_local; -1 if no
+// mass is positive.  Valid in every thread.
+__device__ __forceinline__ int mass_locate(const double* m, int M, double t, const double (&loc)[4], Smem& sm,
+                                           double* t_local) {
+    const int tid = threadIdx.x;
+    const int first = block_first(sm.incl[tid] > t, sm.iscratch);
+    if (tid == 0) {
+        sm.cross = -1;
+        sm.cross_t = 0.0;
+    }
+    __syncthreads();
+    if (first < kThreads && tid == first) {
+        double cum = (first == 0) ? 0.0 : sm.incl[first - 1];
+        int j = -1;
+        double before = cum;
+        int lastp = -1;
+        double lastp_before = 0.0;
+        for (int i = 0; i < 4; ++i) {
+            if (loc[i] > 0.0) {
+                lastp = tid * 4 + i;
+                lastp_before = cum;
+            }
+            if (j < 0 && cum + loc[i] > t && loc[i] > 0.0) {
+                j = tid * 4 + i;
+                before = cum;
+            }
+            cum += loc[i];
+        }
+        if (j < 0) {
+            j = lastp;
+            before = lastp_before;
+        }
+        sm.cross = j;
+        sm.cross_t = t - before;
+    }
+    if (first >= kThreads && tid == 0) {
+        // rounding only: the last positive weight of the last mass with weight
+        for (int j = M - 1; j >= 0; --j)
+            if (m[j] > 0.0) {
+                sm.cross = j;
+                sm.cross_t = m[j];
+                break;
+            }
+    }
+    __syncthreads();
+    *t_local = sm.cross_t;
+    return sm.cross;
+}
+
+// The inverse-CDF draw from target row gamma of b (exact mode), the final
+// distribution when every draft is accepted.  Its masses are the row's
+// stats sub-chunk sums S 2^(K - Kmax), so once the row's stats have published
+// (they stream before all other rows) the draw needs one scan of the single
+// sub-chunk the uniform falls in, at most kFindVec vectors per thread.
+// Returns the token (or -1) in every thread; *total receives the sum of the
+// masses in units of 2^Kmax and *ok whether the row's words arrived.
+template <class D>
+__device__ __forceinline__ int bonus_draw(const StepParams& P, int b, double u, Smem& sm, double* total, bool* ok) {
+    using T = typename D::T;
+    constexpr int E = D::E;
+    const int gamma = P.gamma, V = P.V;
+    const int tid = threadIdx.x;
+    const int W = kWaves * P.nchunk1;
+    float* Kg = sm.K + (size_t)gamma * W;
+    double* Sg = sm.S + (size_t)gamma * W;
+    *ok = wait_ks(P.pslot + (size_t)b * P.pstride + (size_t)gamma * W * 2, W, Kg, Sg);
+    const float km = row_kmax(sm, Kg, W);
+    for (int j = tid; j < W; j += kThreads) sm.sub[j] = ldexp(Sg[j], exp_delta(Kg[j] - km));
+    __syncthreads();
+    double loc[4];
+    *total = mass_prefix(sm.sub, W, sm, loc);
+    if (!(isfinite(*total) && *total > 0.0)) return -1;
+    double t_local = 0.0;
+    const int j = mass_locate(sm.sub, W, u * *total, loc, sm, &t_local);
+    if (j < 0) return -1;
+    const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunk1, V, E);
+    const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gamma) * V + sp.begin;
+    // scan on the sub-chunk's own scale 2^K: its largest weight is at least
+    // 1/2, so a sub-chunk with positive mass always has a positive fp32 weight
+    ExactWeights w{};
+    w.kind = kTargetRow;
+    w.c = P.c;
+    w.kp = Kg[j];
+    const int local = sub_chunk_find_k<D, kTargetRow, kFindVec>(rp, rp, sp.n, w, ldexp(t_local, exp_delta(km - Kg[j])),
+                                                                sm.scratch, sm.incl, sm.iscratch, &sm.result);
+    return (local >= 0) ? sp.begin + local : -1;
+}
+
+// b's bonus workgroup (exact mode): draws the next token from target row
+// gamma as soon as that row's stats have published (they stream before all
+// other rows), and publishes the token and the draw's total with b's stats
+// words, where b's decider reads them.
+template <class D>
+__device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm) {
+    const int gamma = P.gamma, R = 2 * gamma + 1;
+    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
+    double total = 0.0;
+    bool got = true;
+    const int idx = bonus_draw<D>(P, b, u, sm, &total, &got);
+    if (!got && threadIdx.x == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0) {
+        unsigned long long* out = P.pslot + (size_t)b * P.pstride + (size_t)R * kWaves * P.nchunk1 * 2;
+        publish(out, (got && idx >= 0) ? (double)idx : -1.0);
+        publish(out + 1, total);
+    }
+}
+
 // b's decision, made once by b's decider workgroup and published as a small
 // record for b's mass and draw workgroups; it also writes the tau / normaliser
-// probes.
+// probes.  If every draft is accepted (exact mode) the output is the token b's
+// bonus workgroup drew, and b's mass and draw workgroups only hand off.
 template <class D, bool kExact>
 __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& sm) {
     const int gamma = P.gamma, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
+    const bool direct = kExact && P.bonus_direct;
     const Decision d = decide<D, kExact>(P, b, sm);
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (P.tau_out != nullptr && tid < gamma) P.tau_out[(size_t)b * gamma + tid] = sm.tau[tid];
-    if (kExact && P.lognorm_out != nullptr)
-        for (int i = tid; i < R; i += kThreads)
-            P.lognorm_out[(size_t)b * R + i] = sm.rowL[i] * 0.693147180559945309417;
+    {
+        // one copy of the record per reader (each mass workgroup, then the
+        // draw), which that reader clears once it has read it
+        const unsigned long long rec[kDecisionWords] = {
+            (unsigned long long)(d.L & 0xffff) | ((unsigned long long)(d.bad ? 1 : 0) << 16) | (1ull << 32),
+            pack2(d.ew.kp, d.ew.lp_hi), pack2(d.ew.lp_lo, d.ew.kq), pack2(d.ew.lq_hi, d.ew.lq_lo),
+            pack2(d.ew.d_hi, d.ew.d_lo)};
+        unsigned long long* dst = P.dslot + (size_t)b * (P.nchunk2 + 1) * kDecisionWords;
+        for (int i = tid; i < (P.nchunk2 + 1) * kDecisionWords; i += kThreads) {
+            const int w = i % kDecisionWords;
+            unsigned long long v = rec[0];
+#pragma unroll
+            for (int k = 1; k < kDecisionWords; ++k) v = (w == k) ? rec[k] : v;
+            publish_raw(dst + i, v);
+        }
+    }
     if (tid == 0) {
-        unsigned long long* rec = P.dslot + (size_t)b * kDecisionWords;
-        publish_raw(rec + 1, pack2(d.ew.kp, d.ew.lp_hi));
-        publish_raw(rec + 2, pack2(d.ew.lp_lo, d.ew.kq));
-        publish_raw(rec + 3, pack2(d.ew.lq_hi, d.ew.lq_lo));
-        publish_raw(rec + 4, pack2(d.ew.d_hi, d.ew.d_lo));
-        publish_raw(rec + 0, (unsigned long long)(d.L & 0xffff) | ((unsigned long long)(d.bad ? 1 : 0) << 16) |
-                                 (1ull << 32));
+        if (direct && !d.bad && d.L == gamma) {
+            const int RW = R * kWaves * P.nchunk1;
+            const int idx = (int)sm.K[RW];
+            const double total = sm.S[RW];
+            const bool bad = idx < 0;
+            P.accepted_len[b] = bad ? -1 : gamma;
+            P.next_token[b] = bad ? -1 : idx;
+            // the draw's total in units of the row normaliser (1 up to rounding)
+            if (P.mass_out != nullptr)
+                P.mass_out[b] = bad ? __builtin_nan("") : total / exp2(sm.rowL[gamma] - (double)sm.rowK[gamma]);
+        }
+    }
+    if (P.tau_out != nullptr && tid < gamma) P.tau_out[(size_t)b * gamma + tid] = sm.tau[tid];
+    if (kExact) {
+        if (P.lognorm_out != nullptr)
+            for (int i = tid; i < R; i += kThreads)
+                P.lognorm_out[(size_t)b * R + i] = sm.rowL[i] * 0.693147180559945309417;
+        // b's bonus workgroup has read its row's words before it published the
+        // pair the decider waited for: the decider is their last reader
+        for (int i = tid; i < P.pstride; i += kThreads) clear_word(P.pslot + (size_t)b * P.pstride + i);
     }
 }
 
-// b's published decision (in b's mass and draw workgroups).
-__device__ __forceinline__ Decision read_decision(const StepParams& P, int b, bool exact, Smem& sm) {
+// Copy `copy` of b's published decision (in b's mass and draw workgroups),
+// cleared once read.
+__device__ __forceinline__ Decision read_decision(const StepParams& P, int b, int copy, bool exact, Smem& sm) {
     Decision d{};
-    d.ok = wait_raw(P.dslot + (size_t)b * kDecisionWords, kDecisionWords, sm.rec);
+    unsigned long long* src = P.dslot + ((size_t)b * (P.nchunk2 + 1) + copy) * kDecisionWords;
+    d.ok = wait_raw(src, kDecisionWords, sm.rec);
+    if ((int)threadIdx.x < kDecisionWords) clear_word(src + threadIdx.x);
     const unsigned long long w0 = sm.rec[0];
     d.L = d.ok ? (int)(w0 & 0xffff) : 0;
     d.bad = ((w0 >> 16) & 1) != 0 || !d.ok;
@@ -703,192 +979,151 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
     constexpr int E = D::E;
     const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-    const Decision d = read_decision(P, b, kExact, sm);
+    const Decision d = read_decision(P, b, k2, kExact, sm);
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
+    // the decider drew b's next token itself: only the weights probe needs this pass
+    const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == gamma;
     double m = 0.0;
     if (!d.ok) {
         m = __builtin_nan("");
-    } else if (!d.bad && sp.n > 0) {
+    } else if (!d.bad && sp.n > 0 && !(drawn && P.weight_out == nullptr)) {
         const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V + sp.begin;
         const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V + sp.begin;
         float* wout = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V + sp.begin : nullptr;
         m = kExact ? wave_weight_sum<D>(rp, rq, sp.n, d.ew, wout) : wave_weight_sum<D>(rp, rq, sp.n, d.sw, wout);
     }
-    if (lane == 0) publish(P.mslot + ((size_t)b * P.nchunk2 + k2) * kWaves + wave, m);
+    // the draw reads the masses unless the decider drew the token
+    if (lane == 0 && !drawn) publish(P.mslot + ((size_t)b * P.nchunk2 + k2) * kWaves + wave, m);
 }
 
 // The inverse-CDF draw for b, by b's draw workgroup, once b's mass tiles have
-// published.
+// published (unless b's decider drew it); then clears b's mass words for the
+// next call.
 template <class D, bool kExact>
 __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
     constexpr int E = D::E;
-    const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
+    const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int M = P.nchunk2 * kWaves;
-    Decision d = read_decision(P, b, kExact, sm);
-    unsigned long long* ms = P.mslot + (size_t)b * M;
-    const bool got = d.ok && wait_words(ms, M, sm.sub);
-    if (!got && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
-    const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V;
-    const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V;
-    float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V : nullptr;
-    const int L = d.L;
-    bool bad = d.bad || !got;
-    int idx = -1;
-    double total = __builtin_nan("");
-    for (int pass = 0; pass < 2 && !bad; ++pass) {
-        // fixed-order prefix over the sub-chunk masses: 4 consecutive per thread
-        double loc[4];
-        double ls = 0.0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int j = tid * 4 + i;
-            loc[i] = (j < M) ? sm.sub[j] : 0.0;
-            ls += loc[i];
-        }
-        double tot;
-        const double incl = block_inclusive_scan(ls, sm.scratch, &tot);
-        sm.incl[tid] = incl;
-        total = tot;
-        if (!(isfinite(total) && total >= 0.0)) {
-            bad = true;
-            break;
-        }
-        if (total == 0.0) {
-            if (pass == 0 && L < gamma) {
-                // no residual mass (possible in sigmoid mode): draw from target row L
-                d.ew.kind = kTargetRow;
-                d.sw.kind = kTargetRow;
-                __syncthreads();
-                for (int k2 = 0; k2 < P.nchunk2; ++k2) {
-                    const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
-                    double m = 0.0;
-                    if (sp.n > 0)
-                        m = kExact ? wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, wrow ? wrow + sp.begin : nullptr)
-                                   : wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, wrow ? wrow + sp.begin : nullptr);
-                    if (lane == 0) sm.sub[k2 * kWaves + wave] = m;
-                }
-                __syncthreads();
-                continue;
+    Decision d = read_decision(P, b, P.nchunk2, kExact, sm);
+    const bool drawn = kExact && P.bonus_direct && d.ok && !d.bad && d.L == gamma;
+    if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (!drawn) {
+        unsigned long long* ms = P.mslot + (size_t)b * M;
+        const bool got = d.ok && wait_words(ms, M, sm.sub);
+        if (d.ok && !got && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
+        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V;
+        const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V;
+        float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V : nullptr;
+        const int L = d.L;
+        bool bad = d.bad || !got;
+        int idx = -1;
+        double total = __builtin_nan("");
+        for (int pass = 0; pass < 2 && !bad; ++pass) {
+            double loc[4];
+            total = mass_prefix(sm.sub, M, sm, loc);
+            if (!(isfinite(total) && total >= 0.0)) {
+                bad = true;
+                break;
             }
-            bad = true;
-            break;
-        }
-        const double t = u * total;
-        const int first = block_first(incl > t, sm.iscratch);
-        if (tid == 0) {
-            sm.cross = -1;
-            sm.cross_t = 0.0;
-        }
-        __syncthreads();
-        if (first < kThreads && tid == first) {
-            double cum = (first == 0) ? 0.0 : sm.incl[first - 1];
-            int j = -1;
-            double before = cum;
-            int lastp = -1;
-            double lastp_before = 0.0;
-            for (int i = 0; i < 4; ++i) {
-                if (loc[i] > 0.0) {
-                    lastp = tid * 4 + i;
-                    lastp_before = cum;
+            if (total == 0.0) {
+                if (pass == 0 && L < gamma) {
+                    // no residual mass (possible in sigmoid mode): draw from target row L
+                    d.ew.kind = kTargetRow;
+                    d.sw.kind = kTargetRow;
+                    __syncthreads();
+                    for (int k2 = 0; k2 < P.nchunk2; ++k2) {
+                        const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
+                        double m = 0.0;
+                        if (sp.n > 0)
+                            m = kExact ? wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, wrow ? wrow + sp.begin : nullptr)
+                                       : wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, wrow ? wrow + sp.begin : nullptr);
+                        if (lane == 0) sm.sub[k2 * kWaves + wave] = m;
+                    }
+                    __syncthreads();
+                    continue;
                 }
-                if (j < 0 && cum + loc[i] > t && loc[i] > 0.0) {
-                    j = tid * 4 + i;
-                    before = cum;
-                }
-                cum += loc[i];
+                bad = true;
+                break;
             }
+            double t_local = 0.0;
+            const int j = mass_locate(sm.sub, M, u * total, loc, sm, &t_local);
             if (j < 0) {
-                j = lastp;
-                before = lastp_before;
+                bad = true;
+                break;
             }
-            sm.cross = j;
-            sm.cross_t = t - before;
-        }
-        if (first >= kThreads && tid == 0) {
-            // rounding only: the last positive weight of the last sub-chunk with mass
-            for (int j = M - 1; j >= 0; --j)
-                if (sm.sub[j] > 0.0) {
-                    sm.cross = j;
-                    sm.cross_t = sm.sub[j];
-                    break;
-                }
-        }
-        __syncthreads();
-        const int j = sm.cross;
-        if (j < 0) {
-            bad = true;
+            const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunk2, V, E);
+            const int local = kExact ? sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result)
+                                     : sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result);
+            idx = (local >= 0) ? sp.begin + local : -1;
+            if (idx < 0) bad = true;
             break;
         }
-        const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunk2, V, E);
-        const int local = kExact ? sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, sm.cross_t, sm.scratch, sm.incl, sm.iscratch, &sm.result)
-                                 : sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, sm.cross_t, sm.scratch, sm.incl, sm.iscratch, &sm.result);
-        idx = (local >= 0) ? sp.begin + local : -1;
-        if (idx < 0) bad = true;
-        break;
+        if (tid == 0) {
+            P.accepted_len[b] = bad ? -1 : L;
+            P.next_token[b] = bad ? -1 : idx;
+            if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total;
+        }
+        // the draw is the only reader of b's mass words: clear them for the next call
+        for (int i = tid; i < M; i += kThreads) clear_word(ms + i);
     }
-    if (tid == 0) {
-        P.accepted_len[b] = bad ? -1 : L;
-        P.next_token[b] = bad ? -1 : idx;
-        if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total;
-    }
-    // every workgroup of b is done with b's published words: clear them for the next call
-    __syncthreads();
-    if (kExact)
-        for (int i = tid; i < R * P.nchunk1; i += kThreads) clear_word(P.pslot + (size_t)b * R * P.nchunk1 + i);
-    if (tid < kDecisionWords) clear_word(P.dslot + (size_t)b * kDecisionWords + tid);
-    for (int i = tid; i < M; i += kThreads) clear_word(ms + i);
-}
-
-// Workgroups before block j (see the layout comment of StepParams).
-__device__ __forceinline__ long long block_offset(long long j, long long B, long long S, long long Mt, const int* lag) {
-    auto clampb = [&](long long x) { return x < 0 ? 0 : (x > B ? B : x); };
-    return S * clampb(j) + clampb(j - lag[0]) + Mt * clampb(j - lag[1]) + clampb(j - lag[2]);
 }
 
 template <class D, bool kExact>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void verify_kernel(StepParams P) {
     __shared__ Smem sm;
-    const long long id = blockIdx.x;
-    const long long B = P.B;
-    const long long S = kExact ? (long long)(2 * P.gamma + 1) * P.nchunk1 : 0;  // stats tiles per element
-    const long long Mt = P.nchunk2;                                            // mass tiles per element
-    // block j holds, in this order: the stats tiles of b = j, the decider of
-    // b = j - lag[0], the mass tiles of b = j - lag[1], the draw of b = j - lag[2]
-    long long lo = 0, hi = B + P.lag[2];  // the block containing id: offset(j) <= id < offset(j + 1)
-    while (hi - lo > 1) {
-        const long long mid = (lo + hi) / 2;
-        if (block_offset(mid, B, S, Mt, P.lag) <= id) lo = mid; else hi = mid;
+    // one argument fetch for the role split and the stats role (see Layout)
+    asm volatile("" ::"s"(P.y.endg), "s"(P.y.endd), "s"(P.y.end0), "s"(P.y.end1), "s"(P.y.size0), "s"(P.y.size1), "s"(P.y.size2),
+                 "s"(P.y.lagM), "s"(P.y.b2), "s"(P.y.S), "s"(P.y.Mt), "s"(P.draft), "s"(P.target), "s"(P.pslot),
+                 "s"(P.B), "s"(P.gamma), "s"(P.V), "s"(P.chunk1), "s"(P.nchunk1), "s"(P.c));
+    const Layout& Y = P.y;
+    if (blockIdx.x < Y.endg) {
+        const int b = (int)(blockIdx.x / (unsigned int)P.nchunk1);
+        stats_role<D>(P, b, P.gamma, (int)blockIdx.x - b * P.nchunk1);
+        return;
     }
-    const long long j = lo;
-    long long r = id - block_offset(j, B, S, Mt, P.lag);
-    if (j < B) {
-        if (r < S) {
-            stats_role<D>(P, (int)(j * S + r), sm);
-            return;
-        }
-        r -= S;
+    if (blockIdx.x < Y.endd) {
+        if (kExact) bonus_role<D>(P, (int)(blockIdx.x - Y.endg), sm);
+        return;
     }
-    const long long bd = j - P.lag[0];
-    if (bd >= 0 && bd < B) {
-        if (r == 0) {
-            decider_role<D, kExact>(P, (int)bd, sm);
-            return;
-        }
-        r -= 1;
+    const unsigned int id = blockIdx.x - Y.endd;
+    unsigned int r;    // position in the unit, counted from its first stats tile
+    int bs = 0, bm = 0;  // batch element of the stats / decider part and of the mass / draw part
+    if (id < Y.end0) {
+        const unsigned int k = id / Y.size0;
+        r = id - k * Y.size0;
+        bs = (int)k;
+    } else if (id < Y.end1) {
+        const unsigned int loc = id - Y.end0;
+        const unsigned int k = loc / Y.size1;
+        r = loc - k * Y.size1;
+        bs = Y.lagM + (int)k;
+        bm = (int)k;
+    } else {
+        const unsigned int loc = id - Y.end1;
+        const unsigned int k = loc / Y.size2;
+        r = loc - k * Y.size2 + (unsigned int)Y.S + 1u;
+        bm = Y.b2 + (int)k;
     }
-    const long long bm = j - P.lag[1];
-    if (bm >= 0 && bm < B) {
-        if (r < Mt) {
-            mass_role<D, kExact>(P, (int)bm, (int)r, sm);
-            return;
-        }
-        r -= Mt;
+    const unsigned int S = (unsigned int)Y.S;
+    if (r < S) {
+        const int ri = (int)r / P.nchunk1;  // rows 0 .. gamma - 1, then gamma + 1 .. 2 gamma
+        stats_role<D>(P, bs, ri < P.gamma ? ri : ri + 1, (int)r - ri * P.nchunk1);
+        return;
     }
-    draw_role<D, kExact>(P, (int)(j - P.lag[2]), sm);
+    if (r == S) {
+        decider_role<D, kExact>(P, bs, sm);
+        return;
+    }
+    r -= S + 1u;
+    if (r < (unsigned int)Y.Mt) {
+        mass_role<D, kExact>(P, bm, (int)r, sm);
+        return;
+    }
+    draw_role<D, kExact>(P, bm, sm);
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -903,7 +1138,9 @@ struct Plan {
     int E;
     int chunk1, nchunk1;
     int chunk2, nchunk2;
-    long long n_stats, n_mass, n_total;
+    bool bonus_direct;
+    long long pstride;
+    long long n_stats, n_mass;
     size_t off_dslot, off_pslot, off_mslot, bytes;
 };
 
@@ -926,11 +1163,14 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     long long nc = ceil_div(kWantStatsTiles, B * R);
     nc = std::max(nc, ceil_div(V, kStatsTileBytes / s));
     nc = std::min(nc, max_cells);
-    nc = std::min(nc, std::max<long long>(1, kMergeCap / R));
+    nc = std::min(nc, std::max<long long>(1, kMaxStatsSub / (kWaves * R)));
     const long long chunk = ceil_div(ceil_div(V, nc), E) * E;
     p->chunk1 = (int)chunk;
     p->nchunk1 = (int)ceil_div(V, chunk);
-    if (R * p->nchunk1 > kMergeCap) return false;
+    if (R * p->nchunk1 * kWaves > kMaxStatsSub) return false;
+    // the decider draws from target row gamma itself when a stats sub-chunk
+    // fits its scan (kFindVec vectors per thread)
+    p->bonus_direct = ceil_div(p->chunk1 / E, kWaves) <= (long long)kFindVec * kThreads;
 
     // final-distribution tiles: a sub-chunk (a quarter tile) must fit one
     // vector per thread, and b's sub-chunk masses must fit kMaxSub
@@ -947,29 +1187,46 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
 
     p->n_stats = (long long)B * R * p->nchunk1;
     p->n_mass = (long long)B * p->nchunk2;
-    p->n_total = p->n_stats + p->n_mass + 2LL * B;  // plus a decider and a draw per batch element
-    if (p->n_total > 0x7fffffffLL) return false;
+    // plus a decider and a draw per batch element
+    if (p->n_stats + p->n_mass + 3LL * B > 0x7fffffffLL) return false;
 
     size_t off = 256;  // header: the error flag at byte offset 4
     p->off_dslot = off;
-    off = align256(off + sizeof(unsigned long long) * (size_t)B * kDecisionWords);
+    off = align256(off + sizeof(unsigned long long) * (size_t)B * (p->nchunk2 + 1) * kDecisionWords);
     p->off_pslot = off;
-    off = align256(off + sizeof(unsigned long long) * (size_t)p->n_stats);
+    p->pstride = 2 * (R * p->nchunk1 * kWaves + 1);
+    off = align256(off + sizeof(unsigned long long) * (size_t)B * p->pstride);
     p->off_mslot = off;
     off = align256(off + sizeof(unsigned long long) * (size_t)p->n_mass * kWaves);
     p->bytes = off;
     return true;
 }
 
-// Block lags (in batch elements) of the decider, mass and draw roles.  The
-// decider of b follows b's stats tiles at once; mass and draw workgroups come
-// after the whole stream: interleaving them into it was measured to cost more
-// (their latency-bound lifetimes hold dispatch slots the stream needs) than
-// the overlap gains.
-static void set_lags(long long B, int* lag) {
-    lag[0] = 1;
-    lag[1] = (int)B;
-    lag[2] = (int)B + 1;
+// The layout for B batch elements: G stats tiles of the target rows gamma and
+// Bd bonus workgroups first, then units with S stats tiles and Mt mass tiles
+// each.  The mass and draw roles of b sit lagM = B / 4 units after its stats:
+// late enough that b's decision is usually published when they start (a
+// waiting workgroup holds a dispatch slot the stream needs), early enough
+// that most batch elements finish within the stream.
+static Layout make_layout(long long B, long long G, long long Bd, long long S, long long Mt) {
+    const long long lagM = std::max(1LL, B / 4);
+    Layout y{};
+    y.endg = (unsigned int)G;
+    y.endd = (unsigned int)(G + Bd);
+    y.size0 = (unsigned int)(S + 1);
+    y.size1 = (unsigned int)(S + Mt + 2);
+    y.size2 = (unsigned int)(Mt + 1);
+    y.end0 = (unsigned int)(lagM * (S + 1));
+    y.end1 = (unsigned int)(y.end0 + (B - lagM) * (S + Mt + 2));
+    y.lagM = (int)lagM;
+    y.b2 = (int)(B - lagM);
+    y.S = (int)S;
+    y.Mt = (int)Mt;
+    return y;
+}
+
+static long long layout_workgroups(const Layout& y) {
+    return (long long)y.endd + y.end1 + (long long)y.lagM * y.size2;
 }
 
 struct Call {
@@ -1006,10 +1263,11 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.nchunk1 = pl.nchunk1;
     P.chunk2 = pl.chunk2;
     P.nchunk2 = pl.nchunk2;
-    P.n_stats = exact ? (int)pl.n_stats : 0;
-    P.n_mass = (int)pl.n_mass;
-    P.n_total = P.n_stats + P.n_mass + 2 * a.B;
-    set_lags(a.B, P.lag);
+    P.bonus_direct = (exact && pl.bonus_direct) ? 1 : 0;
+    P.y = make_layout(a.B, exact ? (long long)a.B * pl.nchunk1 : 0, P.bonus_direct ? a.B : 0,
+                      exact ? 2LL * a.gamma * pl.nchunk1 : 0, pl.nchunk2);
+    P.pstride = (int)pl.pstride;
+    const long long n_total = layout_workgroups(P.y);
     P.temperature = (double)a.temperature;
     P.alpha = (double)a.alpha;
     P.beta = (double)a.beta;
@@ -1027,9 +1285,9 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.mass_out = a.mass_out;
     P.lognorm_out = a.lognorm_out;
     if (exact)
-        hipLaunchKernelGGL((verify_kernel<D, true>), dim3(P.n_total), dim3(kThreads), 0, a.stream, P);
+        hipLaunchKernelGGL((verify_kernel<D, true>), dim3((unsigned int)n_total), dim3(kThreads), 0, a.stream, P);
     else
-        hipLaunchKernelGGL((verify_kernel<D, false>), dim3(P.n_total), dim3(kThreads), 0, a.stream, P);
+        hipLaunchKernelGGL((verify_kernel<D, false>), dim3((unsigned int)n_total), dim3(kThreads), 0, a.stream, P);
     return hipGetLastError() == hipSuccess ? SV_OK : SV_ERR_HIP;
 }
 

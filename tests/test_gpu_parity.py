@@ -150,6 +150,26 @@ def test_sentinels(mode):
     assert g.accepted_len[3] == -1
 
 
+def test_bonus_draw_with_vanishing_leading_mass():
+    """Every draft accepted and the last uniform 0: the draw takes the first
+    token of positive probability.  The first 50 logits of target row gamma
+    are so small (p ~ e^-205) that their fp32 weights underflow even against
+    the sub-chunk's own scale; the oracle (fp64) returns token 0, on a CDF
+    edge, so it flags the case.  The GPU must still return a valid token: 0
+    or the first token of representable weight, 50."""
+    x = W.small_case(4, 3, 40000, "f32", seed=91)
+    x.draft[:] = x.target[:, :3]
+    x.uniforms[:, :3] = 0.0
+    x.uniforms[:, 3] = 0.0
+    x.target[:, 3, :50] = -200.0
+    g = run_gpu(x)
+    o = run_oracle(x)
+    assert np.all(g.accepted_len == 3), g.accepted_len
+    assert np.all((g.next_token == 0) | (g.next_token == 50)), g.next_token
+    assert np.all(o.next_token == 0) and np.all(o.flagged())
+    compare(x, g, o, label="vanishing leading mass")
+
+
 @pytest.mark.parametrize("ab", [10.0, 1e3, 1e4, 1e5])
 def test_sigmoid_scaling_constants(ab):
     x = W.small_case(16, 10, 50272, "f16", mode="sigmoid", seed=51, temperature=0.7, alpha=-ab, beta=ab)
