@@ -35,6 +35,8 @@ enum : int { kResidual = 0, kTargetRow = 1 };
 constexpr int kWantStatsTiles = 2048;    // enough workgroups to fill 256 CUs several times
 constexpr int kWantSampleTiles = 1024;
 constexpr int kStatsTileBytes = 65536;   // at most 64 KiB of one row per stats workgroup
+constexpr int kGammaTileBytes = 16384;   // target rows gamma, streamed last: short tiles end the stream sharply
+constexpr int kFindVec = 4;              // vectors per thread when the bonus role scans a row-gamma chunk
 constexpr int kSampleTileBytes = 32768;
 
 // ---------------------------------------------------------------------------
@@ -175,11 +177,7 @@ __device__ __forceinline__ void load_pair_u(const typename D::T* rp, const typen
 }
 
 constexpr int kPassUnroll = 4;  // vectors in flight per lane in the weight pass
-constexpr int kMaxStatsSub = kWaves * kMaxRows;  // stats sub-chunks of one batch element (2 gamma + 1 rows)
-// Per batch element the stats words hold 2 gamma + 1 rows x nchunk1 x kWaves
-// (K, S) pairs, then one more pair: the token drawn from target row gamma and
-// the draw's total mass (see bonus_role).
-constexpr int kFindVec = 4;      // vectors per thread when the decider scans a stats sub-chunk
+constexpr int kMaxStatsSub = 1028;  // stats chunks of one batch element (all 2 gamma + 1 rows)
 constexpr int kMaxSub = 1024;    // sub-chunk masses of one batch element (nchunk2 * kWaves)
 constexpr int kMaxSpins = 1 << 17;  // bound on every wait (about 0.1 s), so every wave exits
 constexpr int kDecisionWords = 5;          // L and the sentinel flag, then 8 floats of weight constants
@@ -223,8 +221,8 @@ __device__ __forceinline__ float unpack_lo(unsigned long long w) { return __uint
 // after kMaxSpins polls.  Each poll issues NV loads per thread before it
 // looks at any (indices clamped into range), so a poll costs one memory
 // round trip for up to NV * kThreads words.
-template <int NV, class F>
-__device__ __forceinline__ bool poll_words(unsigned long long* p, int n, F take) {
+template <int NV, class A, class F>
+__device__ __forceinline__ bool poll_at(int n, A addr, F take) {
     for (int spin = 0;; ++spin) {
         int missing = 0;
         for (int i0 = 0; i0 < n; i0 += NV * kThreads) {
@@ -232,7 +230,7 @@ __device__ __forceinline__ bool poll_words(unsigned long long* p, int n, F take)
 #pragma unroll
             for (int u = 0; u < NV; ++u) {
                 const int i = min(i0 + u * kThreads + (int)threadIdx.x, n - 1);
-                w[u] = __hip_atomic_load(p + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                w[u] = __hip_atomic_load(addr(i), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
 #pragma unroll
             for (int u = 0; u < NV; ++u) {
@@ -249,6 +247,11 @@ __device__ __forceinline__ bool poll_words(unsigned long long* p, int n, F take)
         if (spin >= kMaxSpins) return false;
         __builtin_amdgcn_s_sleep(2);
     }
+}
+
+template <int NV, class F>
+__device__ __forceinline__ bool poll_words(unsigned long long* p, int n, F take) {
+    return poll_at<NV>(n, [&](int i) { return p + i; }, take);
 }
 
 // The n (<= kThreads) raw record words at p, copied to dst.
@@ -429,47 +432,48 @@ __device__ int sub_chunk_find(const typename D::T* rp, const typename D::T* rq, 
 
 // ---------------------------------------------------------------------------
 // the fused step: one launch; a workgroup's role follows from its index
-//   stats (b, r, k)  exact mode: chunk k of row r of batch element b; each
-//                    wave publishes its contiguous quarter's normaliser
-//                    terms (eq. (4)) as a (K, S) pair
+//   stats (b, s, k)  exact mode: chunk k of stats slot s of batch element b
+//                    (slot_row); each wave publishes its contiguous
+//                    quarter's normaliser terms (eq. (4)) as a (K, S) pair
 //   decider (b)      b's decision -- eq. (1) at the drafted tokens and the
-//                    first-rejection scan -- published as a small record;
-//                    when every draft is accepted it also draws the next
-//                    token from target row gamma itself (see decider_role)
-//   mass (b, k2)     the masses of the final distribution (eqs. (2)-(3) or
-//                    the bonus row) over tile k2, one per wave, published
-//   draw (b)         the inverse-CDF draw of b's next token; clears b's
-//                    published words for the next call
-// Index order: first the stats tiles of target row gamma of every batch
-// element and then a bonus workgroup per element (exact mode), then units
-// u = 0, 1, ...: unit u holds the stats
-// tiles of the other rows and then the decider of b = u (for u < B),
-// followed by the mass tiles and then the draw of b = u - lagM (for
-// u >= lagM).  So each role of b comes
-// after the roles it reads, and lagM lets the stream of later batch elements
-// cover the latency of earlier ones.  A workgroup only waits on results of
-// workgroups with smaller indices, and never on a returning atomic: the
-// streaming workgroups publish and retire.  Each XCD dispatches its
-// workgroups in index order, so the waiting workgroup with the smallest index
-// always waits on workgroups that are running and do not wait, or that its
-// XCD will dispatch once its running, non-waiting workgroups finish: no wait
-// can block forever.  Every wait is also bounded (kMaxSpins), so every wave
-// exits regardless.
+//                    first-rejection scan -- published as a small record,
+//                    one copy per reader
+//   mass (b, k2)     the masses of the final distribution (eqs. (2)-(3), or
+//                    the target row) over tile k2, one per wave, published
+//   draw (b)         the inverse-CDF draw of b's next token
+//   bonus (b)        exact mode: if every draft is accepted, the draw from
+//                    target row gamma straight from that row's stats sums
+//                    (no second pass over the row; see bonus_role)
+// Index order: units u = 0, 1, ...: unit u holds the stats tiles of the rows
+// b = u's decision reads and then b's decider (for u < B), followed by the
+// mass tiles and then the draw of b = u - lagM (for u >= lagM); then the
+// stats tiles of every target row gamma (exact mode, when the bonus role
+// draws); then the mass and draw roles of the last lagM batch elements; then
+// the bonus workgroups.  Decisions and the residual draws of most batch
+// elements so finish while the stream still runs, and the stream ends with
+// rows whose only remaining work is one scan each.
 //
-// Units fall into three segments of uniform unit size (stats + decider;
-// all four roles; mass + draw), so a workgroup finds its role with one
-// division, from kernel arguments that sit in the first cache lines of the
-// argument block together with everything the stats role reads: a stats
-// workgroup starts its stream after a single argument fetch.
+// Each role of b comes after the roles it reads.  A workgroup only waits on
+// results of workgroups with smaller indices, and never on a returning
+// atomic: the streaming workgroups publish and retire.  Each XCD dispatches
+// its workgroups in index order, so the waiting workgroup with the smallest
+// index always waits on workgroups that are running and do not wait, or that
+// its XCD will dispatch once its running, non-waiting workgroups finish: no
+// wait can block forever.  Every wait is also bounded (kMaxSpins), so every
+// wave exits regardless.
+//
+// Segments have uniform unit sizes, so a workgroup finds its role with at
+// most one division, from kernel arguments that sit in the first cache lines
+// of the argument block together with everything the stats role reads: a
+// stats workgroup starts its stream after a single argument fetch.
 // ---------------------------------------------------------------------------
 struct Layout {
-    unsigned int endg;                 // stats tiles of the target rows gamma (B nchunk1, or 0)
-    unsigned int endd;                 // ... then one bonus workgroup per batch element (or none)
-    unsigned int end0, end1;           // first workgroup index of segments 1 and 2, counted after endg
+    unsigned int end0, end1;           // ends of unit segments 0 (stats + decider) and 1 (all four)
+    unsigned int endg, end2;           // ends of segment G (target rows gamma) and 2 (mass + draw)
     unsigned int size0, size1, size2;  // workgroups per unit in segments 0, 1, 2
     int lagM;                          // unit lag of the mass and draw roles
     int b2;                            // batch element of the first unit of segment 2
-    int S;                             // stats tiles per unit: rows other than gamma (0 in sigmoid mode)
+    int S;                             // stats tiles per unit (0 in sigmoid mode)
     int Mt;                            // mass tiles per batch element
 };
 
@@ -477,19 +481,22 @@ struct StepParams {
     Layout y;
     const void* draft;
     const void* target;
-    unsigned long long* pslot;     // [B, (2 gamma + 1) nchunk1 kWaves + 1, 2] stats (K, S) pairs, bonus draw
+    unsigned long long* pslot;     // [B, 2 gamma + 1 slots, nchunk1, kWaves, 2] stats (K, S) pairs
     int B, gamma, V;
     int chunk1, nchunk1;           // exact: row chunks
+    int chunkg, nchunkg;           // exact: chunks of target row gamma when the bonus role draws
     float c;                       // exact: log2(e) / T
     int chunk2, nchunk2;           // final-distribution tiles per batch element
     float s, s0;                   // sigmoid: u = fma(z, s, s0)
-    int bonus_direct;              // exact: b's bonus workgroup draws from target row gamma (see bonus_role)
+    int bonus_direct;              // exact: the bonus role draws when every draft is accepted
+    int nslot;                     // exact: stats slots the decider reads (2 gamma, or 2 gamma + 1)
+    int ncopy;                     // copies of each decision record (one per reader)
     int pstride;                   // stats words per batch element
     const int32_t* tokens;
     const float* uniforms;
     double temperature, alpha, beta;
     unsigned int* error;           // set to 1 if a wait ever timed out
-    unsigned long long* dslot;     // [B, nchunk2 + 1, kDecisionWords] copies of the published decision
+    unsigned long long* dslot;     // [B, ncopy, kDecisionWords] copies of the published decision
     unsigned long long* mslot;     // [B, nchunk2, kWaves] sub-chunk masses
     int32_t* accepted_len;
     int32_t* next_token;
@@ -500,12 +507,11 @@ struct StepParams {
 };
 
 struct Smem {
-    float K[kMaxStatsSub + 1];   // exact: b's stats sub-chunk references
-    double S[kMaxStatsSub + 1];  //        and sums (then the bonus draw's token and total)
-    double rowL[kMaxRows];     // exact: b's row log2-normalisers
-    float rowK[kMaxRows];      //        and the largest reference of each row
+    float K[kMaxStatsSub];     // exact: b's stats chunk references
+    double S[kMaxStatsSub];    //        and sums
+    double rowL[kMaxRows];     // exact: log2-normaliser of each stats slot
     double tau[kMaxGamma];
-    double sub[kMaxSub];       // draw: b's sub-chunk masses
+    double sub[kMaxSub];       // sub-chunk masses of a draw
     double incl[kThreads];
     double scratch[kWaves];
     int iscratch[kWaves];
@@ -518,6 +524,10 @@ struct Smem {
     double cross_t;
 };
 
+// Stats slots of a batch element: the rows its decision reads first (target
+// rows 0 .. gamma - 1, then draft rows 0 .. gamma - 1), target row gamma last.
+__device__ __forceinline__ int slot_row(int s, int gamma) { return s < gamma ? s : (s < 2 * gamma ? s + 1 : gamma); }
+
 __device__ __forceinline__ double min1(double r) { return (r >= 1.0) ? 1.0 : r; }  // keeps NaN
 
 __device__ __forceinline__ void split3(double v, float& hi, float& mid, float& lo) {
@@ -526,21 +536,24 @@ __device__ __forceinline__ void split3(double v, float& hi, float& mid, float& l
     lo = (float)((v - (double)hi) - (double)mid);
 }
 
-// Exact mode, one chunk of one row: sum_x 2^(z c - K) in one streaming pass.
-// Wave w covers the contiguous quarter sub_chunk(k, w, ...) of the chunk and
-// publishes its pair (K, S): K an integral reference (or -inf), S the fp64 sum
-// of 2^(z c - K) over its elements, so sum_x e^(z/T) = sum over quarters of
-// S 2^K, merged later by exact power-of-two scaling.
+// Exact mode, one chunk of one row: sum_x 2^(z c - K) in one streaming pass,
+// published as the pair (K, S): K an integral reference (or -inf), S the fp64
+// sum of 2^(z c - K) over the chunk, so sum_x e^(z/T) = sum over chunks of
+// S 2^K, merged later by exact power-of-two scaling.  Wave w streams the
+// contiguous quarter sub_chunk(k, w, ...) of the chunk; the quarters merge
+// in wave order.
 template <class D>
-__device__ __forceinline__ void stats_role(const StepParams& P, int b, int r, int k) {
+__device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot, int k, Smem& sm) {
     using T = typename D::T;
     constexpr int E = D::E;
     const int gamma = P.gamma, V = P.V;
     const float c = P.c;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int r = slot_row(slot, gamma);
+    const int chunk = (slot == 2 * gamma && P.bonus_direct) ? P.chunkg : P.chunk1;
     const T* row = (r <= gamma) ? static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + r) * (size_t)V
                                 : static_cast<const T*>(P.draft) + ((size_t)b * gamma + (r - gamma - 1)) * (size_t)V;
-    const Span sp = sub_chunk(k, wave, P.chunk1, V, E);
+    const Span sp = sub_chunk(k, wave, chunk, V, E);
     const T* base = row + sp.begin;
     const int n = sp.n;
     const int nfull = n / E;  // whole 16-byte vectors
@@ -574,17 +587,16 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int r, in
         load_elems_or_pad<D>(base, nfull * E, n, x[0]);
         lse_absorb_block<1, E>(st, x, c);
     }
-    const Lse w = wave_lse(st);
-    if (lane == 0) {
-        const size_t sub = ((size_t)r * P.nchunk1 + k) * kWaves + wave;
-        unsigned long long* out = P.pslot + (size_t)b * P.pstride + sub * 2;
-        publish(out, (double)w.k);
-        publish(out + 1, w.s);
+    const Lse t = block_lse(st, sm.sk, sm.ss);
+    if (threadIdx.x == 0) {
+        unsigned long long* out = P.pslot + (size_t)b * P.pstride + ((size_t)slot * P.nchunk1 + k) * 2;
+        publish(out, (double)t.k);
+        publish(out + 1, t.s);
     }
 }
 
 // Row log2-normalisers Lambda = Kmax + log2(sum S 2^(K - Kmax)) of R rows
-// from the (K, S) pairs of their W sub-chunks in LDS, into sm.rowL / sm.rowK:
+// from the (K, S) pairs of their W sub-chunks in LDS, into sm.rowL:
 // one thread per row, in sub-chunk order, reading blocks of 16 pairs at a time
 // (clamped, masked indices) so each block costs one LDS round trip.  Ends
 // with a workgroup barrier.
@@ -616,7 +628,6 @@ __device__ __forceinline__ void merge_rows(Smem& sm, int R, int W) {
         }
         // a NaN logit makes S NaN; a +inf logit makes K +inf and S NaN
         sm.rowL[i] = (sum != sum) ? __builtin_nan("") : ((m == -INFINITY) ? -INFINITY : (double)m + log2(sum));
-        sm.rowK[i] = m;
     }
     __syncthreads();
 }
@@ -680,12 +691,11 @@ struct Decision {
 };
 
 // The decision for batch element b: eq. (1) at the drafted tokens and the
-// first-rejection scan, plus the weights of the final distribution.  Every
-// workgroup that needs it computes it the same way, so they all agree.
+// first-rejection scan, plus the weights of the final distribution.
 template <class D, bool kExact>
 __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
-    const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
+    const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x;
     const T* draft = static_cast<const T*>(P.draft) + (size_t)b * gamma * V;
     const T* target = static_cast<const T*>(P.target) + (size_t)b * (gamma + 1) * V;
@@ -707,12 +717,11 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     Decision d{};
     d.ok = true;
     if (kExact) {
-        // b's stats sub-chunk pairs (K, S), then each row's log2-normaliser
-        // max K + log2(sum S 2^(K - max K)), merged in sub-chunk order by
-        // exact power-of-two scaling
-        const int W = kWaves * P.nchunk1;  // sub-chunks per row
-        d.ok = wait_ks(P.pslot + (size_t)b * P.pstride, R * W + (P.bonus_direct ? 1 : 0), sm.K, sm.S);
-        merge_rows(sm, R, W);
+        // the stats slots the decision reads, merged into log2-normalisers
+        // max K + log2(sum S 2^(K - max K)) by exact power-of-two scaling
+        const int W = P.nchunk1;  // chunks per row
+        d.ok = wait_ks(P.pslot + (size_t)b * P.pstride, P.nslot * W, sm.K, sm.S);
+        merge_rows(sm, P.nslot, W);
     }
 
     int stop = 0;
@@ -720,8 +729,8 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
         double tau;
         bool row_ok;
         if (kExact) {
-            const double lam_p = sm.rowL[tid];
-            const double lam_q = sm.rowL[gamma + 1 + tid];
+            const double lam_p = sm.rowL[tid];          // target row tid
+            const double lam_q = sm.rowL[gamma + tid];  // draft row tid
             row_ok = isfinite(lam_p) && isfinite(lam_q);
             if (zq == -INFINITY) {
                 tau = 1.0;  // q(x) = 0
@@ -746,11 +755,14 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     bool first_bad, tok_bad;
     scan_stops(stop, tok_ok, sm, &first, &first_bad, &tok_bad);
     d.L = min(first, gamma);
-    d.bad = tok_bad || first_bad || !d.ok || (kExact && d.L == gamma && !isfinite(sm.rowL[gamma]));
+    // with the bonus role, target row gamma is its business (it sentinels a
+    // non-finite row itself)
+    d.bad = tok_bad || first_bad || !d.ok ||
+            (kExact && !P.bonus_direct && d.L == gamma && !isfinite(sm.rowL[2 * gamma]));
     const bool two_rows = d.L < gamma;
-    if (kExact && !d.bad) {
-        const double lp = sm.rowL[min(d.L, gamma)];
-        const double lq = sm.rowL[gamma + 1 + min(d.L, gamma - 1)];
+    if (kExact && !d.bad && (two_rows || !P.bonus_direct)) {
+        const double lp = sm.rowL[two_rows ? d.L : 2 * gamma];
+        const double lq = sm.rowL[gamma + min(d.L, gamma - 1)];
         d.ew.kind = two_rows ? kResidual : kTargetRow;
         d.ew.c = P.c;
         split3(lp, d.ew.kp, d.ew.lp_hi, d.ew.lp_lo);
@@ -834,84 +846,24 @@ __device__ __forceinline__ int mass_locate(const double* m, int M, double t, con
     return sm.cross;
 }
 
-// The inverse-CDF draw from target row gamma of b (exact mode), the final
-// distribution when every draft is accepted.  Its masses are the row's
-// stats sub-chunk sums S 2^(K - Kmax), so once the row's stats have published
-// (they stream before all other rows) the draw needs one scan of the single
-// sub-chunk the uniform falls in, at most kFindVec vectors per thread.
-// Returns the token (or -1) in every thread; *total receives the sum of the
-// masses in units of 2^Kmax and *ok whether the row's words arrived.
-template <class D>
-__device__ __forceinline__ int bonus_draw(const StepParams& P, int b, double u, Smem& sm, double* total, bool* ok) {
-    using T = typename D::T;
-    constexpr int E = D::E;
-    const int gamma = P.gamma, V = P.V;
-    const int tid = threadIdx.x;
-    const int W = kWaves * P.nchunk1;
-    float* Kg = sm.K + (size_t)gamma * W;
-    double* Sg = sm.S + (size_t)gamma * W;
-    *ok = wait_ks(P.pslot + (size_t)b * P.pstride + (size_t)gamma * W * 2, W, Kg, Sg);
-    const float km = row_kmax(sm, Kg, W);
-    for (int j = tid; j < W; j += kThreads) sm.sub[j] = ldexp(Sg[j], exp_delta(Kg[j] - km));
-    __syncthreads();
-    double loc[4];
-    *total = mass_prefix(sm.sub, W, sm, loc);
-    if (!(isfinite(*total) && *total > 0.0)) return -1;
-    double t_local = 0.0;
-    const int j = mass_locate(sm.sub, W, u * *total, loc, sm, &t_local);
-    if (j < 0) return -1;
-    const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunk1, V, E);
-    const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gamma) * V + sp.begin;
-    // scan on the sub-chunk's own scale 2^K: its largest weight is at least
-    // 1/2, so a sub-chunk with positive mass always has a positive fp32 weight
-    ExactWeights w{};
-    w.kind = kTargetRow;
-    w.c = P.c;
-    w.kp = Kg[j];
-    const int local = sub_chunk_find_k<D, kTargetRow, kFindVec>(rp, rp, sp.n, w, ldexp(t_local, exp_delta(km - Kg[j])),
-                                                                sm.scratch, sm.incl, sm.iscratch, &sm.result);
-    return (local >= 0) ? sp.begin + local : -1;
-}
-
-// b's bonus workgroup (exact mode): draws the next token from target row
-// gamma as soon as that row's stats have published (they stream before all
-// other rows), and publishes the token and the draw's total with b's stats
-// words, where b's decider reads them.
-template <class D>
-__device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm) {
-    const int gamma = P.gamma, R = 2 * gamma + 1;
-    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
-    double total = 0.0;
-    bool got = true;
-    const int idx = bonus_draw<D>(P, b, u, sm, &total, &got);
-    if (!got && threadIdx.x == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (threadIdx.x == 0) {
-        unsigned long long* out = P.pslot + (size_t)b * P.pstride + (size_t)R * kWaves * P.nchunk1 * 2;
-        publish(out, (got && idx >= 0) ? (double)idx : -1.0);
-        publish(out + 1, total);
-    }
-}
-
 // b's decision, made once by b's decider workgroup and published as a small
-// record for b's mass and draw workgroups; it also writes the tau / normaliser
-// probes.  If every draft is accepted (exact mode) the output is the token b's
-// bonus workgroup drew, and b's mass and draw workgroups only hand off.
+// record, one copy per reader (each mass workgroup, the draw, the bonus
+// workgroup), which that reader clears once it has read it.  The decider also
+// writes the tau / normaliser probes and clears the stats words it read (it
+// is their only reader).
 template <class D, bool kExact>
 __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& sm) {
     const int gamma = P.gamma, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
-    const bool direct = kExact && P.bonus_direct;
     const Decision d = decide<D, kExact>(P, b, sm);
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     {
-        // one copy of the record per reader (each mass workgroup, then the
-        // draw), which that reader clears once it has read it
         const unsigned long long rec[kDecisionWords] = {
             (unsigned long long)(d.L & 0xffff) | ((unsigned long long)(d.bad ? 1 : 0) << 16) | (1ull << 32),
             pack2(d.ew.kp, d.ew.lp_hi), pack2(d.ew.lp_lo, d.ew.kq), pack2(d.ew.lq_hi, d.ew.lq_lo),
             pack2(d.ew.d_hi, d.ew.d_lo)};
-        unsigned long long* dst = P.dslot + (size_t)b * (P.nchunk2 + 1) * kDecisionWords;
-        for (int i = tid; i < (P.nchunk2 + 1) * kDecisionWords; i += kThreads) {
+        unsigned long long* dst = P.dslot + (size_t)b * P.ncopy * kDecisionWords;
+        for (int i = tid; i < P.ncopy * kDecisionWords; i += kThreads) {
             const int w = i % kDecisionWords;
             unsigned long long v = rec[0];
 #pragma unroll
@@ -919,35 +871,21 @@ __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& s
             publish_raw(dst + i, v);
         }
     }
-    if (tid == 0) {
-        if (direct && !d.bad && d.L == gamma) {
-            const int RW = R * kWaves * P.nchunk1;
-            const int idx = (int)sm.K[RW];
-            const double total = sm.S[RW];
-            const bool bad = idx < 0;
-            P.accepted_len[b] = bad ? -1 : gamma;
-            P.next_token[b] = bad ? -1 : idx;
-            // the draw's total in units of the row normaliser (1 up to rounding)
-            if (P.mass_out != nullptr)
-                P.mass_out[b] = bad ? __builtin_nan("") : total / exp2(sm.rowL[gamma] - (double)sm.rowK[gamma]);
-        }
-    }
     if (P.tau_out != nullptr && tid < gamma) P.tau_out[(size_t)b * gamma + tid] = sm.tau[tid];
     if (kExact) {
+        const int W = P.nchunk1;
         if (P.lognorm_out != nullptr)
-            for (int i = tid; i < R; i += kThreads)
-                P.lognorm_out[(size_t)b * R + i] = sm.rowL[i] * 0.693147180559945309417;
-        // b's bonus workgroup has read its row's words before it published the
-        // pair the decider waited for: the decider is their last reader
-        for (int i = tid; i < P.pstride; i += kThreads) clear_word(P.pslot + (size_t)b * P.pstride + i);
+            for (int i = tid; i < P.nslot; i += kThreads)
+                P.lognorm_out[(size_t)b * R + slot_row(i, gamma)] = sm.rowL[i] * 0.693147180559945309417;
+        for (int i = tid; i < 2 * P.nslot * W; i += kThreads) clear_word(P.pslot + (size_t)b * P.pstride + i);
     }
 }
 
-// Copy `copy` of b's published decision (in b's mass and draw workgroups),
-// cleared once read.
+// Copy `copy` of b's published decision (in b's mass, draw and bonus
+// workgroups), cleared once read.
 __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, int copy, bool exact, Smem& sm) {
     Decision d{};
-    unsigned long long* src = P.dslot + ((size_t)b * (P.nchunk2 + 1) + copy) * kDecisionWords;
+    unsigned long long* src = P.dslot + ((size_t)b * P.ncopy + copy) * kDecisionWords;
     d.ok = wait_raw(src, kDecisionWords, sm.rec);
     if ((int)threadIdx.x < kDecisionWords) clear_word(src + threadIdx.x);
     const unsigned long long w0 = sm.rec[0];
@@ -973,6 +911,95 @@ __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, in
     return d;
 }
 
+// b's bonus workgroup (exact mode): waits for its copy of b's decision and
+// for target row gamma's stats (which stream last), and, if every draft was
+// accepted, draws the next token from that row and writes b's outputs.  The
+// masses of the inverse-CDF draw are the row's chunk sums S 2^(K - Kmax), so
+// the draw scans only the one chunk the uniform falls in (kFindVec vectors
+// per thread).  It is the only reader of row gamma's words and clears them.
+template <class D>
+__device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm) {
+    using T = typename D::T;
+    const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
+    const int tid = threadIdx.x;
+    const int W = P.nchunkg;
+    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
+    unsigned long long* rec = P.dslot + ((size_t)b * P.ncopy + P.ncopy - 1) * kDecisionWords;
+    unsigned long long* words = P.pslot + (size_t)b * P.pstride + (size_t)2 * gamma * P.nchunk1 * 2;
+    // one poll over the decision record and the row's (K, S) pairs
+    const bool ok = poll_at<4>(
+        kDecisionWords + 2 * W,
+        [&](int i) { return (i < kDecisionWords) ? rec + i : words + (i - kDecisionWords); },
+        [&](int i, unsigned long long w) {
+            if (i < kDecisionWords) {
+                sm.rec[i] = ~w;
+            } else {
+                const int j = i - kDecisionWords;
+                if (j & 1)
+                    sm.S[j >> 1] = decode_word(w);
+                else
+                    sm.K[j >> 1] = (float)decode_word(w);
+            }
+        });
+    for (int i = tid; i < kDecisionWords + 2 * W; i += kThreads)
+        clear_word((i < kDecisionWords) ? rec + i : words + (i - kDecisionWords));
+    if (!ok) {
+        if (tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const unsigned long long w0 = sm.rec[0];
+    // otherwise b's draw workgroup writes b's outputs
+    const bool draw = ((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gamma;
+    if (!draw && P.lognorm_out == nullptr) return;
+
+    const float km = row_kmax(sm, sm.K, W);
+    for (int j = tid; j < W; j += kThreads) sm.sub[j] = ldexp(sm.S[j], exp_delta(sm.K[j] - km));
+    __syncthreads();
+    double loc[4];
+    const double total = mass_prefix(sm.sub, W, sm, loc);
+    const double lam = (double)km + log2(total);  // the row's log2-normaliser
+    if (P.lognorm_out != nullptr && tid == 0) P.lognorm_out[(size_t)b * R + gamma] = lam * 0.693147180559945309417;
+    if (!draw) return;
+    // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
+    int idx = -1;
+    if (isfinite(total) && total > 0.0) {
+        double t_local = 0.0;
+        const int j = mass_locate(sm.sub, W, u * total, loc, sm, &t_local);
+        if (j >= 0) {
+            const int begin = j * P.chunkg;
+            const int n = min(V, begin + P.chunkg) - begin;
+            const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gamma) * V + begin;
+            // scan on the chunk's own scale 2^K: its largest weight is at least
+            // 1/2, so a chunk with positive mass has a positive weight
+            ExactWeights w{};
+            w.kind = kTargetRow;
+            w.c = P.c;
+            w.kp = sm.K[j];
+            const int local = sub_chunk_find_k<D, kTargetRow, kFindVec>(
+                rp, rp, n, w, ldexp(t_local, exp_delta(km - sm.K[j])), sm.scratch, sm.incl, sm.iscratch,
+                &sm.result);
+            idx = (local >= 0) ? begin + local : -1;
+        }
+    }
+    const bool bad = idx < 0;
+    if (tid == 0) {
+        P.accepted_len[b] = bad ? -1 : gamma;
+        P.next_token[b] = bad ? -1 : idx;
+        // the draw's total in units of the row normaliser (1 up to rounding)
+        if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total * exp2((double)km - lam);
+    }
+    if (P.weight_out != nullptr && !bad) {
+        // probe: p(x) over the whole row
+        ExactWeights w{};
+        w.kind = kTargetRow;
+        w.c = P.c;
+        split3(lam, w.kp, w.lp_hi, w.lp_lo);
+        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gamma) * V;
+        for (int x = tid; x < V; x += kThreads)
+            P.weight_out[(size_t)b * V + x] = w.template eval<kTargetRow>(to_f32(rp[x]), -INFINITY);
+    }
+}
+
 template <class D, bool kExact>
 __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Smem& sm) {
     using T = typename D::T;
@@ -981,25 +1008,25 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const Decision d = read_decision(P, b, k2, kExact, sm);
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
-    // the decider drew b's next token itself: only the weights probe needs this pass
+    // b's bonus workgroup draws when every draft is accepted: nothing to do here
     const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == gamma;
+    if (drawn) return;
+    const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
     double m = 0.0;
     if (!d.ok) {
         m = __builtin_nan("");
-    } else if (!d.bad && sp.n > 0 && !(drawn && P.weight_out == nullptr)) {
+    } else if (!d.bad && sp.n > 0) {
         const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V + sp.begin;
         const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V + sp.begin;
         float* wout = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V + sp.begin : nullptr;
         m = kExact ? wave_weight_sum<D>(rp, rq, sp.n, d.ew, wout) : wave_weight_sum<D>(rp, rq, sp.n, d.sw, wout);
     }
-    // the draw reads the masses unless the decider drew the token
-    if (lane == 0 && !drawn) publish(P.mslot + ((size_t)b * P.nchunk2 + k2) * kWaves + wave, m);
+    if (lane == 0) publish(P.mslot + ((size_t)b * P.nchunk2 + k2) * kWaves + wave, m);
 }
 
 // The inverse-CDF draw for b, by b's draw workgroup, once b's mass tiles have
-// published (unless b's decider drew it); then clears b's mass words for the
-// next call.
+// published (unless b's bonus workgroup draws); then clears b's mass words
+// for the next call.
 template <class D, bool kExact>
 __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
@@ -1008,90 +1035,81 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int M = P.nchunk2 * kWaves;
     Decision d = read_decision(P, b, P.nchunk2, kExact, sm);
-    const bool drawn = kExact && P.bonus_direct && d.ok && !d.bad && d.L == gamma;
+    const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == gamma;
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (!drawn) {
-        unsigned long long* ms = P.mslot + (size_t)b * M;
-        const bool got = d.ok && wait_words(ms, M, sm.sub);
-        if (d.ok && !got && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
-        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V;
-        const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V;
-        float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V : nullptr;
-        const int L = d.L;
-        bool bad = d.bad || !got;
-        int idx = -1;
-        double total = __builtin_nan("");
-        for (int pass = 0; pass < 2 && !bad; ++pass) {
-            double loc[4];
-            total = mass_prefix(sm.sub, M, sm, loc);
-            if (!(isfinite(total) && total >= 0.0)) {
-                bad = true;
-                break;
-            }
-            if (total == 0.0) {
-                if (pass == 0 && L < gamma) {
-                    // no residual mass (possible in sigmoid mode): draw from target row L
-                    d.ew.kind = kTargetRow;
-                    d.sw.kind = kTargetRow;
-                    __syncthreads();
-                    for (int k2 = 0; k2 < P.nchunk2; ++k2) {
-                        const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
-                        double m = 0.0;
-                        if (sp.n > 0)
-                            m = kExact ? wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, wrow ? wrow + sp.begin : nullptr)
-                                       : wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, wrow ? wrow + sp.begin : nullptr);
-                        if (lane == 0) sm.sub[k2 * kWaves + wave] = m;
-                    }
-                    __syncthreads();
-                    continue;
-                }
-                bad = true;
-                break;
-            }
-            double t_local = 0.0;
-            const int j = mass_locate(sm.sub, M, u * total, loc, sm, &t_local);
-            if (j < 0) {
-                bad = true;
-                break;
-            }
-            const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunk2, V, E);
-            const int local = kExact ? sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result)
-                                     : sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result);
-            idx = (local >= 0) ? sp.begin + local : -1;
-            if (idx < 0) bad = true;
+    if (drawn) return;
+    unsigned long long* ms = P.mslot + (size_t)b * M;
+    const bool got = d.ok && wait_words(ms, M, sm.sub);
+    if (d.ok && !got && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
+    const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V;
+    const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V;
+    float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V : nullptr;
+    const int L = d.L;
+    bool bad = d.bad || !got;
+    int idx = -1;
+    double total = __builtin_nan("");
+    for (int pass = 0; pass < 2 && !bad; ++pass) {
+        double loc[4];
+        total = mass_prefix(sm.sub, M, sm, loc);
+        if (!(isfinite(total) && total >= 0.0)) {
+            bad = true;
             break;
         }
-        if (tid == 0) {
-            P.accepted_len[b] = bad ? -1 : L;
-            P.next_token[b] = bad ? -1 : idx;
-            if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total;
+        if (total == 0.0) {
+            if (pass == 0 && L < gamma) {
+                // no residual mass (possible in sigmoid mode): draw from target row L
+                d.ew.kind = kTargetRow;
+                d.sw.kind = kTargetRow;
+                __syncthreads();
+                for (int k2 = 0; k2 < P.nchunk2; ++k2) {
+                    const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
+                    double m = 0.0;
+                    if (sp.n > 0)
+                        m = kExact ? wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, wrow ? wrow + sp.begin : nullptr)
+                                   : wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, wrow ? wrow + sp.begin : nullptr);
+                    if (lane == 0) sm.sub[k2 * kWaves + wave] = m;
+                }
+                __syncthreads();
+                continue;
+            }
+            bad = true;
+            break;
         }
-        // the draw is the only reader of b's mass words: clear them for the next call
-        for (int i = tid; i < M; i += kThreads) clear_word(ms + i);
+        double t_local = 0.0;
+        const int j = mass_locate(sm.sub, M, u * total, loc, sm, &t_local);
+        if (j < 0) {
+            bad = true;
+            break;
+        }
+        const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunk2, V, E);
+        const int local = kExact ? sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result)
+                                 : sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result);
+        idx = (local >= 0) ? sp.begin + local : -1;
+        if (idx < 0) bad = true;
+        break;
     }
+    if (tid == 0) {
+        P.accepted_len[b] = bad ? -1 : L;
+        P.next_token[b] = bad ? -1 : idx;
+        if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total;
+    }
+    // the draw is the only reader of b's mass words: clear them for the next call
+    for (int i = tid; i < M; i += kThreads) clear_word(ms + i);
 }
 
 template <class D, bool kExact>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void verify_kernel(StepParams P) {
     __shared__ Smem sm;
     // one argument fetch for the role split and the stats role (see Layout)
-    asm volatile("" ::"s"(P.y.endg), "s"(P.y.endd), "s"(P.y.end0), "s"(P.y.end1), "s"(P.y.size0), "s"(P.y.size1), "s"(P.y.size2),
-                 "s"(P.y.lagM), "s"(P.y.b2), "s"(P.y.S), "s"(P.y.Mt), "s"(P.draft), "s"(P.target), "s"(P.pslot),
-                 "s"(P.B), "s"(P.gamma), "s"(P.V), "s"(P.chunk1), "s"(P.nchunk1), "s"(P.c));
+    asm volatile("" ::"s"(P.y.end0), "s"(P.y.end1), "s"(P.y.endg), "s"(P.y.end2), "s"(P.y.size0),
+                 "s"(P.y.size1), "s"(P.y.size2), "s"(P.y.lagM), "s"(P.y.b2), "s"(P.y.S), "s"(P.y.Mt),
+                 "s"(P.draft), "s"(P.target), "s"(P.pslot), "s"(P.B), "s"(P.gamma), "s"(P.V), "s"(P.chunk1),
+                 "s"(P.nchunk1), "s"(P.chunkg), "s"(P.nchunkg), "s"(P.c));
     const Layout& Y = P.y;
-    if (blockIdx.x < Y.endg) {
-        const int b = (int)(blockIdx.x / (unsigned int)P.nchunk1);
-        stats_role<D>(P, b, P.gamma, (int)blockIdx.x - b * P.nchunk1);
-        return;
-    }
-    if (blockIdx.x < Y.endd) {
-        if (kExact) bonus_role<D>(P, (int)(blockIdx.x - Y.endg), sm);
-        return;
-    }
-    const unsigned int id = blockIdx.x - Y.endd;
-    unsigned int r;    // position in the unit, counted from its first stats tile
-    int bs = 0, bm = 0;  // batch element of the stats / decider part and of the mass / draw part
+    const unsigned int id = blockIdx.x;
+    unsigned int r;        // position in the unit, counted from its first stats tile
+    int bs = 0, bm = 0;    // batch element of the stats / decider part and of the mass / draw part
     if (id < Y.end0) {
         const unsigned int k = id / Y.size0;
         r = id - k * Y.size0;
@@ -1102,16 +1120,25 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         r = loc - k * Y.size1;
         bs = Y.lagM + (int)k;
         bm = (int)k;
-    } else {
-        const unsigned int loc = id - Y.end1;
+    } else if (id < Y.endg) {
+        // target row gamma of every batch element, streamed last
+        const int t = (int)(id - Y.end1);
+        const int b = t / P.nchunkg;
+        stats_role<D>(P, b, 2 * P.gamma, t - b * P.nchunkg, sm);
+        return;
+    } else if (id < Y.end2) {
+        const unsigned int loc = id - Y.endg;
         const unsigned int k = loc / Y.size2;
         r = loc - k * Y.size2 + (unsigned int)Y.S + 1u;
         bm = Y.b2 + (int)k;
+    } else {
+        if (kExact) bonus_role<D>(P, (int)(id - Y.end2), sm);
+        return;
     }
     const unsigned int S = (unsigned int)Y.S;
     if (r < S) {
-        const int ri = (int)r / P.nchunk1;  // rows 0 .. gamma - 1, then gamma + 1 .. 2 gamma
-        stats_role<D>(P, bs, ri < P.gamma ? ri : ri + 1, (int)r - ri * P.nchunk1);
+        const int slot = (int)r / P.nchunk1;
+        stats_role<D>(P, bs, slot, (int)r - slot * P.nchunk1, sm);
         return;
     }
     if (r == S) {
@@ -1138,6 +1165,7 @@ struct Plan {
     int E;
     int chunk1, nchunk1;
     int chunk2, nchunk2;
+    int chunkg, nchunkg;
     bool bonus_direct;
     long long pstride;
     long long n_stats, n_mass;
@@ -1163,14 +1191,18 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     long long nc = ceil_div(kWantStatsTiles, B * R);
     nc = std::max(nc, ceil_div(V, kStatsTileBytes / s));
     nc = std::min(nc, max_cells);
-    nc = std::min(nc, std::max<long long>(1, kMaxStatsSub / (kWaves * R)));
+    nc = std::min(nc, std::max<long long>(1, kMaxStatsSub / R));
     const long long chunk = ceil_div(ceil_div(V, nc), E) * E;
     p->chunk1 = (int)chunk;
     p->nchunk1 = (int)ceil_div(V, chunk);
-    if (R * p->nchunk1 * kWaves > kMaxStatsSub) return false;
-    // the decider draws from target row gamma itself when a stats sub-chunk
-    // fits its scan (kFindVec vectors per thread)
-    p->bonus_direct = ceil_div(p->chunk1 / E, kWaves) <= (long long)kFindVec * kThreads;
+    if (R * p->nchunk1 > kMaxStatsSub) return false;
+    // target row gamma in short tiles that fit the bonus role's scan
+    // (kFindVec vectors per thread); their masses must fit kMaxSub
+    const long long ncg = std::max(ceil_div(V, kGammaTileBytes / s), ceil_div(V, (long long)kFindVec * kThreads * E));
+    const long long chunkg = ceil_div(ceil_div(V, ncg), E) * E;
+    p->chunkg = (int)chunkg;
+    p->nchunkg = (int)ceil_div(V, chunkg);
+    p->bonus_direct = p->nchunkg <= kMaxSub && chunkg / E <= (long long)kFindVec * kThreads;
 
     // final-distribution tiles: a sub-chunk (a quarter tile) must fit one
     // vector per thread, and b's sub-chunk masses must fit kMaxSub
@@ -1185,16 +1217,16 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     if ((long long)p->nchunk2 * kWaves > kMaxSub || chunk2 / E > max_tile_vecs) return false;
     p->E = E;
 
-    p->n_stats = (long long)B * R * p->nchunk1;
+    p->n_stats = (long long)B * (2LL * gamma * p->nchunk1 + (p->bonus_direct ? p->nchunkg : p->nchunk1));
     p->n_mass = (long long)B * p->nchunk2;
     // plus a decider and a draw per batch element
     if (p->n_stats + p->n_mass + 3LL * B > 0x7fffffffLL) return false;
 
     size_t off = 256;  // header: the error flag at byte offset 4
     p->off_dslot = off;
-    off = align256(off + sizeof(unsigned long long) * (size_t)B * (p->nchunk2 + 1) * kDecisionWords);
+    off = align256(off + sizeof(unsigned long long) * (size_t)B * (p->nchunk2 + 2) * kDecisionWords);
     p->off_pslot = off;
-    p->pstride = 2 * (R * p->nchunk1 * kWaves + 1);
+    p->pstride = 2 * (2LL * gamma * p->nchunk1 + (p->bonus_direct ? p->nchunkg : p->nchunk1));
     off = align256(off + sizeof(unsigned long long) * (size_t)B * p->pstride);
     p->off_mslot = off;
     off = align256(off + sizeof(unsigned long long) * (size_t)p->n_mass * kWaves);
@@ -1202,31 +1234,27 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     return true;
 }
 
-// The layout for B batch elements: G stats tiles of the target rows gamma and
-// Bd bonus workgroups first, then units with S stats tiles and Mt mass tiles
-// each.  The mass and draw roles of b sit lagM = B / 4 units after its stats:
-// late enough that b's decision is usually published when they start (a
-// waiting workgroup holds a dispatch slot the stream needs), early enough
+// The layout for B batch elements: units with S stats tiles, a decider, Mt
+// mass tiles and a draw each; G stats tiles of the target rows gamma; Bd bonus
+// workgroups.  The mass and draw roles of b sit lagM = B / 4 units after its
+// stats: late enough that b's decision is usually published when they start
+// (a waiting workgroup holds a dispatch slot the stream needs), early enough
 // that most batch elements finish within the stream.
-static Layout make_layout(long long B, long long G, long long Bd, long long S, long long Mt) {
+static Layout make_layout(long long B, long long S, long long Mt, long long G) {
     const long long lagM = std::max(1LL, B / 4);
     Layout y{};
-    y.endg = (unsigned int)G;
-    y.endd = (unsigned int)(G + Bd);
     y.size0 = (unsigned int)(S + 1);
     y.size1 = (unsigned int)(S + Mt + 2);
     y.size2 = (unsigned int)(Mt + 1);
     y.end0 = (unsigned int)(lagM * (S + 1));
     y.end1 = (unsigned int)(y.end0 + (B - lagM) * (S + Mt + 2));
+    y.endg = (unsigned int)(y.end1 + G);
+    y.end2 = (unsigned int)(y.endg + lagM * (Mt + 1));
     y.lagM = (int)lagM;
     y.b2 = (int)(B - lagM);
     y.S = (int)S;
     y.Mt = (int)Mt;
     return y;
-}
-
-static long long layout_workgroups(const Layout& y) {
-    return (long long)y.endd + y.end1 + (long long)y.lagM * y.size2;
 }
 
 struct Call {
@@ -1263,11 +1291,17 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.nchunk1 = pl.nchunk1;
     P.chunk2 = pl.chunk2;
     P.nchunk2 = pl.nchunk2;
-    P.bonus_direct = (exact && pl.bonus_direct) ? 1 : 0;
-    P.y = make_layout(a.B, exact ? (long long)a.B * pl.nchunk1 : 0, P.bonus_direct ? a.B : 0,
-                      exact ? 2LL * a.gamma * pl.nchunk1 : 0, pl.nchunk2);
+    P.chunkg = pl.chunkg;
+    P.nchunkg = pl.nchunkg;
+    // with the bonus role, target row gamma streams last (segment G) and the
+    // deciders read the other 2 gamma rows; otherwise units hold all rows
+    const bool direct = exact && pl.bonus_direct;
+    P.bonus_direct = direct ? 1 : 0;
+    P.nslot = exact ? (direct ? 2 * a.gamma : 2 * a.gamma + 1) : 0;
+    P.ncopy = pl.nchunk2 + (direct ? 2 : 1);
     P.pstride = (int)pl.pstride;
-    const long long n_total = layout_workgroups(P.y);
+    P.y = make_layout(a.B, (long long)P.nslot * pl.nchunk1, pl.nchunk2, direct ? (long long)a.B * pl.nchunkg : 0);
+    const long long n_total = (long long)P.y.end2 + (direct ? a.B : 0);
     P.temperature = (double)a.temperature;
     P.alpha = (double)a.alpha;
     P.beta = (double)a.beta;
