@@ -98,11 +98,12 @@ typedef enum sv_status {
  * Bytes of device workspace a call with these sizes needs (the same value
  * serves both modes).  Returns 0 for invalid sizes, including vocabularies
  * above 2^20 (fp32) or 2^21 (fp16 / bf16) entries.  The workspace holds the
- * per-chunk row log-normalisers (exact mode) and the per-chunk masses of the
- * final distribution.  The 32-bit word at byte offset 4 becomes nonzero if a
- * wait between workgroups ever times out (about 0.1 s), which would indicate
- * a fault; results of that call are sentinels and the workspace must be
- * re-initialised.
+ * per-chunk normaliser partials (exact mode), one copy of each batch
+ * element's decision per workgroup that reads it, and the per-chunk masses of
+ * the final distribution.  The 32-bit word at byte offset 4 becomes nonzero
+ * if a wait between workgroups ever times out (about 0.1 s), which would
+ * indicate a fault; the outputs of that call are then not valid and the
+ * workspace must be re-initialised.
  */
 size_t spec_verify_workspace_bytes(int32_t batch, int32_t gamma, int32_t vocab, sv_dtype_t dtype);
 
