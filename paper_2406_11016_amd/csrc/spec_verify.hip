@@ -952,19 +952,60 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     const bool draw = ((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gamma;
     if (!draw && P.lognorm_out == nullptr) return;
 
-    const float km = row_kmax(sm, sm.K, W);
-    for (int j = tid; j < W; j += kThreads) sm.sub[j] = ldexp(sm.S[j], exp_delta(sm.K[j] - km));
-    __syncthreads();
-    double loc[4];
-    const double total = mass_prefix(sm.sub, W, sm, loc);
+    // the masses S 2^(K - Kmax) of the row's chunks, their total and the chunk
+    // the uniform falls in
+    float km;
+    double total, t_local;
+    int j;
+    if (W <= kWave) {
+        // one wave: a butterfly maximum and a shuffle scan, one barrier
+        if (tid < kWave) {
+            const float K = (tid < W) ? sm.K[tid] : -INFINITY;
+            const double S = (tid < W) ? sm.S[tid] : 0.0;
+            const float m0 = wave_max(K);
+            const double m = ldexp(S, exp_delta(K - m0));
+            double incl = m;
+#pragma unroll
+            for (int o = 1; o < kWave; o <<= 1) {
+                const double nb = __shfl_up(incl, o, kWave);
+                if (tid >= o) incl += nb;
+            }
+            const double up1 = __shfl_up(incl, 1, kWave);  // every lane takes part in the shuffle
+            const double excl = (tid == 0) ? 0.0 : up1;
+            const double tot = __shfl(incl, kWave - 1, kWave);
+            const double t = u * tot;
+            const unsigned long long over = __ballot(incl > t && m > 0.0);
+            const unsigned long long pos = __ballot(m > 0.0);
+            // first chunk whose running sum exceeds t; if rounding leaves t at
+            // or beyond the total, the last chunk with mass
+            const int jj = over ? __ffsll((long long)over) - 1 : (pos ? 63 - __clzll((long long)pos) : -1);
+            if (tid == 0) {
+                sm.kmax = m0;
+                sm.scratch[0] = tot;
+                sm.cross = jj;
+            }
+            if (jj >= 0 && tid == jj) sm.cross_t = over ? t - excl : m;
+        }
+        __syncthreads();
+        km = sm.kmax;
+        total = sm.scratch[0];
+        j = sm.cross;
+        t_local = sm.cross_t;
+    } else {
+        km = row_kmax(sm, sm.K, W);
+        for (int i = tid; i < W; i += kThreads) sm.sub[i] = ldexp(sm.S[i], exp_delta(sm.K[i] - km));
+        __syncthreads();
+        double loc[4];
+        total = mass_prefix(sm.sub, W, sm, loc);
+        t_local = 0.0;
+        j = mass_locate(sm.sub, W, u * total, loc, sm, &t_local);
+    }
     const double lam = (double)km + log2(total);  // the row's log2-normaliser
     if (P.lognorm_out != nullptr && tid == 0) P.lognorm_out[(size_t)b * R + gamma] = lam * 0.693147180559945309417;
     if (!draw) return;
     // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
     int idx = -1;
     if (isfinite(total) && total > 0.0) {
-        double t_local = 0.0;
-        const int j = mass_locate(sm.sub, W, u * total, loc, sm, &t_local);
         if (j >= 0) {
             const int begin = j * P.chunkg;
             const int n = min(V, begin + P.chunkg) - begin;
@@ -1210,6 +1251,7 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     long long nc2 = ceil_div(kWantSampleTiles, B);
     nc2 = std::max(nc2, ceil_div(V, kSampleTileBytes / s));
     nc2 = std::min(nc2, max_cells);
+    nc2 = std::min(nc2, (long long)kMaxSub / kWaves);
     nc2 = std::max(nc2, ceil_div(V, max_tile_vecs * E));
     const long long chunk2 = ceil_div(ceil_div(V, nc2), E) * E;
     p->chunk2 = (int)chunk2;

@@ -60,6 +60,18 @@ def test_workspace_bytes(lib):
         assert f(*bad) == 0
 
 
+def test_workspace_bytes_small_batches_large_vocabularies(lib):
+    """Every batch size plans the largest vocabularies the header allows
+    (2^20 fp32, 2^21 fp16/bf16) and rejects the next size up."""
+    f = lib.spec_verify_workspace_bytes
+    for B in (1, 2, 3, 5, 17, 64):
+        for gamma in (1, 8, 128):
+            for V, dt in ((300007, 0), (1 << 20, 0), (600011, 2), (1 << 21, 1), (1 << 21, 2)):
+                assert f(B, gamma, V, dt) > 0, (B, gamma, V, dt)
+            assert f(B, gamma, (1 << 20) + 1, 0) == 0
+            assert f(B, gamma, (1 << 21) + 1, 2) == 0
+
+
 def _args(**kw):
     base = dict(draft=0x1000, target=0x2000, dtype=0, tokens=0x3000, uniforms=0x4000, B=2, gamma=3, V=100,
                 T=1.0, acc=0x5000, nxt=0x6000, ws=0x7000, ws_bytes=1 << 20, stream=None)

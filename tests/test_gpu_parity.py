@@ -170,6 +170,16 @@ def test_bonus_draw_with_vanishing_leading_mass():
     compare(x, g, o, label="vanishing leading mass")
 
 
+@pytest.mark.parametrize("dtype,V", [("f32", 300007), ("bf16", 600011)])
+def test_bonus_draw_over_many_row_tiles(dtype, V):
+    """Target row gamma spans more than 64 of its 16 KiB tiles, so the draw
+    locates its tile with the workgroup-wide scan; drafts equal to the
+    target rows make every draft accepted."""
+    x = W.small_case(3, 2, V, dtype, seed=93)
+    x.draft[:] = x.target[:, :2]
+    compare(x, run_gpu(x), run_oracle(x), label=f"many row tiles {dtype}")
+
+
 @pytest.mark.parametrize("ab", [10.0, 1e3, 1e4, 1e5])
 def test_sigmoid_scaling_constants(ab):
     x = W.small_case(16, 10, 50272, "f16", mode="sigmoid", seed=51, temperature=0.7, alpha=-ab, beta=ab)
