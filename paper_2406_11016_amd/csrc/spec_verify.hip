@@ -467,7 +467,18 @@ __device__ int sub_chunk_find(const typename D::T* rp, const typename D::T* rq, 
 // of the argument block together with everything the stats role reads: a
 // stats workgroup starts its stream after a single argument fetch.
 // ---------------------------------------------------------------------------
+// n / d for 0 <= n < 2^31 as one 32 x 32 -> 64-bit multiply and a shift:
+// with L = ceil(log2 d) and m = floor(2^(31+L) / d) + 1 (< 2^32), the error of
+// n m / 2^(31+L) over n / d is below 2^-L <= 1/d, so the floor is exact.
+struct Div {
+    unsigned int m, sh;
+    __device__ __forceinline__ unsigned int of(unsigned int n) const {
+        return (unsigned int)(((unsigned long long)n * m) >> sh);
+    }
+};
+
 struct Layout {
+    Div d0, d1, d2, dc1, dcg;          // division by size0, size1, size2, nchunk1, nchunkg
     unsigned int end0, end1;           // ends of unit segments 0 (stats + decider) and 1 (all four)
     unsigned int endg, end2;           // ends of segment G (target rows gamma) and 2 (mass + draw)
     unsigned int size0, size1, size2;  // workgroups per unit in segments 0, 1, 2
@@ -1143,7 +1154,8 @@ template <class D, bool kExact>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void verify_kernel(StepParams P) {
     __shared__ Smem sm;
     // one argument fetch for the role split and the stats role (see Layout)
-    asm volatile("" ::"s"(P.y.end0), "s"(P.y.end1), "s"(P.y.endg), "s"(P.y.end2), "s"(P.y.size0),
+    asm volatile("" ::"s"(P.y.d0.m), "s"(P.y.d0.sh), "s"(P.y.d1.m), "s"(P.y.d1.sh), "s"(P.y.dc1.m),
+                 "s"(P.y.dc1.sh), "s"(P.y.end0), "s"(P.y.end1), "s"(P.y.endg), "s"(P.y.end2), "s"(P.y.size0),
                  "s"(P.y.size1), "s"(P.y.size2), "s"(P.y.lagM), "s"(P.y.b2), "s"(P.y.S), "s"(P.y.Mt),
                  "s"(P.draft), "s"(P.target), "s"(P.pslot), "s"(P.B), "s"(P.gamma), "s"(P.V), "s"(P.chunk1),
                  "s"(P.nchunk1), "s"(P.chunkg), "s"(P.nchunkg), "s"(P.c));
@@ -1152,24 +1164,24 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     unsigned int r;        // position in the unit, counted from its first stats tile
     int bs = 0, bm = 0;    // batch element of the stats / decider part and of the mass / draw part
     if (id < Y.end0) {
-        const unsigned int k = id / Y.size0;
+        const unsigned int k = Y.d0.of(id);
         r = id - k * Y.size0;
         bs = (int)k;
     } else if (id < Y.end1) {
         const unsigned int loc = id - Y.end0;
-        const unsigned int k = loc / Y.size1;
+        const unsigned int k = Y.d1.of(loc);
         r = loc - k * Y.size1;
         bs = Y.lagM + (int)k;
         bm = (int)k;
     } else if (id < Y.endg) {
         // target row gamma of every batch element, streamed last
         const int t = (int)(id - Y.end1);
-        const int b = t / P.nchunkg;
+        const int b = (int)Y.dcg.of((unsigned int)t);
         stats_role<D>(P, b, 2 * P.gamma, t - b * P.nchunkg, sm);
         return;
     } else if (id < Y.end2) {
         const unsigned int loc = id - Y.endg;
-        const unsigned int k = loc / Y.size2;
+        const unsigned int k = Y.d2.of(loc);
         r = loc - k * Y.size2 + (unsigned int)Y.S + 1u;
         bm = Y.b2 + (int)k;
     } else {
@@ -1178,7 +1190,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     }
     const unsigned int S = (unsigned int)Y.S;
     if (r < S) {
-        const int slot = (int)r / P.nchunk1;
+        const int slot = (int)Y.dc1.of(r);
         stats_role<D>(P, bs, slot, (int)r - slot * P.nchunk1, sm);
         return;
     }
@@ -1282,7 +1294,14 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
 // stats: late enough that b's decision is usually published when they start
 // (a waiting workgroup holds a dispatch slot the stream needs), early enough
 // that most batch elements finish within the stream.
-static Layout make_layout(long long B, long long S, long long Mt, long long G) {
+static Div make_div(unsigned int d) {
+    unsigned int L = 0;
+    while ((1ull << L) < d) ++L;
+    const unsigned long long m = ((1ull << (31 + L)) / d) + 1;
+    return Div{(unsigned int)m, 31 + L};
+}
+
+static Layout make_layout(long long B, long long S, long long Mt, long long G, int nchunk1, int nchunkg) {
     const long long lagM = std::max(1LL, B / 4);
     Layout y{};
     y.size0 = (unsigned int)(S + 1);
@@ -1296,6 +1315,11 @@ static Layout make_layout(long long B, long long S, long long Mt, long long G) {
     y.b2 = (int)(B - lagM);
     y.S = (int)S;
     y.Mt = (int)Mt;
+    y.d0 = make_div(y.size0);
+    y.d1 = make_div(y.size1);
+    y.d2 = make_div(y.size2);
+    y.dc1 = make_div((unsigned int)std::max(1, nchunk1));
+    y.dcg = make_div((unsigned int)std::max(1, nchunkg));
     return y;
 }
 
@@ -1342,7 +1366,8 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.nslot = exact ? (direct ? 2 * a.gamma : 2 * a.gamma + 1) : 0;
     P.ncopy = pl.nchunk2 + (direct ? 2 : 1);
     P.pstride = (int)pl.pstride;
-    P.y = make_layout(a.B, (long long)P.nslot * pl.nchunk1, pl.nchunk2, direct ? (long long)a.B * pl.nchunkg : 0);
+    P.y = make_layout(a.B, (long long)P.nslot * pl.nchunk1, pl.nchunk2, direct ? (long long)a.B * pl.nchunkg : 0,
+                      pl.nchunk1, pl.nchunkg);
     const long long n_total = (long long)P.y.end2 + (direct ? a.B : 0);
     P.temperature = (double)a.temperature;
     P.alpha = (double)a.alpha;
