@@ -89,6 +89,36 @@ def cpu_baseline(w, x, min_seconds: float):
                       f"({reps} repetitions, {el:.1f} s, single thread), scaled to whole steps"}
 
 
+def unfused_baseline(w, sets, tok, uni, steps: int, warmup: int):
+    """The same step with stock PyTorch operators (one eager kernel per
+    operator, fp32 probabilities), timed with HIP events on the current stream
+    over the same rotating inputs."""
+    import torch
+
+    from paper_2406_11016_amd import unfused_torch
+    nrot = len(sets)
+
+    def step(i):
+        d, t = sets[i % nrot]
+        return unfused_torch.verify(d, t, tok, uni, mode=w.mode, temperature=w.temperature, alpha=w.alpha,
+                                    beta=w.beta)
+
+    for i in range(warmup):
+        step(i)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for i in range(steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    return {"value": round(1000.0 / ms, 1), "unit": "verify-steps/s", "ms_per_step": round(ms, 6),
+            "steps": steps, "what": "stock PyTorch operators on the same GPU and inputs: softmax/sigmoid, gather, "
+                                    "eq. (1), cumprod scan, residual, cumsum + searchsorted (fp32)"}
+
+
 def copy_calibration(nbytes: int, reps: int) -> None:
     """A plain device-to-device copy of known size, for scaling HBM counters."""
     import torch
@@ -112,6 +142,7 @@ def main() -> int:
                          "(defeats the 256 MB last-level cache)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-unfused", action="store_true", help="skip timing the unfused PyTorch comparison")
     ap.add_argument("--copy-calibration-mb", type=float, default=0.0,
                     help="only run a plain copy of this size (for counter calibration) and exit")
     args = ap.parse_args()
@@ -188,6 +219,12 @@ def main() -> int:
                 "kernel": "verify_kernel<exact> (the whole step is one launch)" if w.mode == "exact"
                 else "verify_kernel<sigmoid> (the whole step is one launch)", "algorithmic_bytes_per_step": alg}
 
+    unfused = None
+    if not args.no_unfused:
+        log("timing the unfused PyTorch comparison")
+        unfused = unfused_baseline(w, sets, tok, uni, steps=max(20, min(200, args.steps // 10)), warmup=5)
+        unfused["speedup_of_fused"] = round(steps_per_s / unfused["value"], 2)
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"timing the CPU oracle for ~{args.cpu_seconds:.0f} s")
@@ -202,6 +239,7 @@ def main() -> int:
                    "logits": w.dtype, "temperature": w.temperature, "rotating_copies": nrot},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "unfused_torch": unfused,
     }
     print(json.dumps(out), flush=True)
     return 0

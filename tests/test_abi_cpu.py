@@ -129,6 +129,8 @@ def test_probe_entry_points_validate_too(lib):
 def test_no_cpu_fallback_in_binding():
     src = open(os.path.join(ROOT, "paper_2406_11016_amd", "binding.py")).read()
     assert "oracle" not in src
+    # the unfused PyTorch comparison is never a fallback of the library
+    assert "unfused" not in src
     for f in os.listdir(os.path.join(ROOT, "paper_2406_11016_amd")):
         if f.endswith(".py"):
             assert "import oracle" not in open(os.path.join(ROOT, "paper_2406_11016_amd", f)).read()
