@@ -36,7 +36,6 @@ constexpr int kWantStatsTiles = 2048;    // enough workgroups to fill 256 CUs se
 constexpr int kWantSampleTiles = 1024;
 constexpr int kStatsTileBytes = 65536;   // at most 64 KiB of one row per stats workgroup
 constexpr int kGammaTileBytes = 16384;   // target rows gamma, streamed last: short tiles end the stream sharply
-constexpr int kFindVec = 4;              // vectors per thread when the bonus role scans a row-gamma chunk
 constexpr int kSampleTileBytes = 32768;
 
 // ---------------------------------------------------------------------------
@@ -598,6 +597,18 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot,
         load_elems_or_pad<D>(base, nfull * E, n, x[0]);
         lse_absorb_block<1, E>(st, x, c);
     }
+    if (slot == 2 * gamma && P.bonus_direct) {
+        // target row gamma: one pair per wave, so the bonus draw scans a
+        // single quarter (one vector per thread)
+        const Lse w = wave_lse(st);
+        if (lane == 0) {
+            unsigned long long* out =
+                P.pslot + (size_t)b * P.pstride + ((size_t)slot * P.nchunk1 + (size_t)k * kWaves + wave) * 2;
+            publish(out, (double)w.k);
+            publish(out + 1, w.s);
+        }
+        return;
+    }
     const Lse t = block_lse(st, sm.sk, sm.ss);
     if (threadIdx.x == 0) {
         unsigned long long* out = P.pslot + (size_t)b * P.pstride + ((size_t)slot * P.nchunk1 + k) * 2;
@@ -925,15 +936,15 @@ __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, in
 // b's bonus workgroup (exact mode): waits for its copy of b's decision and
 // for target row gamma's stats (which stream last), and, if every draft was
 // accepted, draws the next token from that row and writes b's outputs.  The
-// masses of the inverse-CDF draw are the row's chunk sums S 2^(K - Kmax), so
-// the draw scans only the one chunk the uniform falls in (kFindVec vectors
-// per thread).  It is the only reader of row gamma's words and clears them.
+// masses of the inverse-CDF draw are the sums S 2^(K - Kmax) of the row's
+// tile quarters, so the draw scans only the one quarter the uniform falls in
+// (one vector per thread).  It is the only reader of row gamma's words and clears them.
 template <class D>
 __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
     const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
-    const int W = P.nchunkg;
+    const int W = kWaves * P.nchunkg;  // quarters of the row's tiles
     const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
     unsigned long long* rec = P.dslot + ((size_t)b * P.ncopy + P.ncopy - 1) * kDecisionWords;
     unsigned long long* words = P.pslot + (size_t)b * P.pstride + (size_t)2 * gamma * P.nchunk1 * 2;
@@ -1018,16 +1029,17 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     int idx = -1;
     if (isfinite(total) && total > 0.0) {
         if (j >= 0) {
-            const int begin = j * P.chunkg;
-            const int n = min(V, begin + P.chunkg) - begin;
+            const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunkg, V, D::E);
+            const int begin = sp.begin;
+            const int n = sp.n;
             const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gamma) * V + begin;
-            // scan on the chunk's own scale 2^K: its largest weight is at least
-            // 1/2, so a chunk with positive mass has a positive weight
+            // scan on the quarter's own scale 2^K: its largest weight is at
+            // least 1/2, so a quarter with positive mass has a positive weight
             ExactWeights w{};
             w.kind = kTargetRow;
             w.c = P.c;
             w.kp = sm.K[j];
-            const int local = sub_chunk_find_k<D, kTargetRow, kFindVec>(
+            const int local = sub_chunk_find_k<D, kTargetRow, 1>(
                 rp, rp, n, w, ldexp(t_local, exp_delta(km - sm.K[j])), sm.scratch, sm.incl, sm.iscratch,
                 &sm.result);
             idx = (local >= 0) ? begin + local : -1;
@@ -1249,13 +1261,13 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     p->chunk1 = (int)chunk;
     p->nchunk1 = (int)ceil_div(V, chunk);
     if (R * p->nchunk1 > kMaxStatsSub) return false;
-    // target row gamma in short tiles that fit the bonus role's scan
-    // (kFindVec vectors per thread); their masses must fit kMaxSub
-    const long long ncg = std::max(ceil_div(V, kGammaTileBytes / s), ceil_div(V, (long long)kFindVec * kThreads * E));
+    // target row gamma in short tiles whose quarters fit the bonus role's scan
+    // (one vector per thread); the quarters' masses must fit kMaxSub
+    const long long ncg = std::max(ceil_div(V, kGammaTileBytes / s), ceil_div(V, (long long)kWaves * kThreads * E));
     const long long chunkg = ceil_div(ceil_div(V, ncg), E) * E;
     p->chunkg = (int)chunkg;
     p->nchunkg = (int)ceil_div(V, chunkg);
-    p->bonus_direct = p->nchunkg <= kMaxSub && chunkg / E <= (long long)kFindVec * kThreads;
+    p->bonus_direct = (long long)p->nchunkg * kWaves <= kMaxSub && ceil_div(chunkg / E, kWaves) <= kThreads;
 
     // final-distribution tiles: a sub-chunk (a quarter tile) must fit one
     // vector per thread, and b's sub-chunk masses must fit kMaxSub
@@ -1280,7 +1292,7 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     p->off_dslot = off;
     off = align256(off + sizeof(unsigned long long) * (size_t)B * (p->nchunk2 + 2) * kDecisionWords);
     p->off_pslot = off;
-    p->pstride = 2 * (2LL * gamma * p->nchunk1 + (p->bonus_direct ? p->nchunkg : p->nchunk1));
+    p->pstride = 2 * (2LL * gamma * p->nchunk1 + (p->bonus_direct ? (long long)kWaves * p->nchunkg : p->nchunk1));
     off = align256(off + sizeof(unsigned long long) * (size_t)B * p->pstride);
     p->off_mslot = off;
     off = align256(off + sizeof(unsigned long long) * (size_t)p->n_mass * kWaves);
