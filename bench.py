@@ -67,26 +67,144 @@ def recorded_traffic(workload: str):
     return None if w is None else int(w["traffic_bytes"])
 
 
-def cpu_baseline(w, x, min_seconds: float):
-    """The oracle as it stands, timed on a bounded sample of the same inputs."""
+_POOL_INPUTS = None
+
+
+def _single_thread_blas() -> None:
+    from threadpoolctl import threadpool_limits
+    threadpool_limits(1)
+
+
+def _oracle_on(x, lo: int, hi: int) -> int:
     import numpy as np
 
     import oracle
+    with np.errstate(all="ignore"):
+        oracle.verify(x.draft[lo:hi], x.target[lo:hi], x.tokens[lo:hi], x.uniforms[lo:hi], dtype=x.dtype,
+                      mode=x.mode, temperature=x.temperature, alpha=x.alpha, beta=x.beta)
+    return hi - lo
+
+
+def _oracle_element(b: int) -> int:
+    return _oracle_on(_POOL_INPUTS, b, b + 1)
+
+
+def host_description() -> dict:
+    import numpy as np
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_count": os.cpu_count(), "usable_cores": len(os.sched_getaffinity(0)), "cpu_model": model,
+            "numpy": np.__version__}
+
+
+def cpu_baseline(w, x, min_seconds: float, max_workers: int = 16):
+    """The oracle as it stands, timed on the host: (i) one thread on a bounded
+    sample of batch elements, scaled to whole steps; (ii) a process pool over
+    the batch elements of whole steps, one worker per usable core (at most
+    ``max_workers``), each worker single-threaded.
+
+    Must run before the process touches the GPU: the pool forks."""
+    import multiprocessing as mp
+
+    from threadpoolctl import threadpool_limits
+    global _POOL_INPUTS
+
     nb = min(w.batch, 16)
-    sl = slice(0, nb)
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        with np.errstate(all="ignore"):
-            oracle.verify(x.draft[sl], x.target[sl], x.tokens[sl], x.uniforms[sl], dtype=x.dtype, mode=x.mode,
-                          temperature=x.temperature, alpha=x.alpha, beta=x.beta)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= min_seconds:
-            break
-    steps_per_s = reps * nb / w.batch / el
-    return {"value": steps_per_s, "unit": "verify-steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"float64 NumPy oracle on batch elements 0..{nb - 1} of {w.batch} "
-                      f"({reps} repetitions, {el:.1f} s, single thread), scaled to whole steps"}
+    with threadpool_limits(1):
+        _oracle_on(x, 0, 1)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            for b in range(nb):
+                _oracle_on(x, b, b + 1)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= min_seconds:
+                break
+    single = {"value": reps * nb / w.batch / el, "unit": "verify-steps/s", "cores": 1, "kind": "oracle",
+              "sample": f"float64 NumPy oracle on batch elements 0..{nb - 1} of {w.batch} "
+                        f"one element per call ({reps} repetitions, {el:.1f} s, one thread), scaled to whole steps"}
+
+    workers = max(1, min(len(os.sched_getaffinity(0)), max_workers, w.batch))
+    _POOL_INPUTS = x
+    try:
+        with mp.get_context("fork").Pool(workers, initializer=_single_thread_blas) as pool:
+            pool.map(_oracle_element, range(min(w.batch, workers)), chunksize=1)   # start-up, imports
+            steps, t0 = 0, time.perf_counter()
+            while True:
+                pool.map(_oracle_element, range(w.batch), chunksize=1)
+                steps += 1
+                el = time.perf_counter() - t0
+                if el >= min_seconds:
+                    break
+    finally:
+        _POOL_INPUTS = None
+    out = {"value": steps / el, "unit": "verify-steps/s", "cores": workers, "kind": "oracle",
+           "sample": f"float64 NumPy oracle over all {w.batch} batch elements of {steps} whole steps "
+                     f"({el:.1f} s), a process pool of {workers} single-threaded workers, one batch "
+                     f"element per task"}
+    out["single_thread"] = single
+    out["host"] = host_description()
+    return out
+
+
+def latency_percentiles(step, calls: int, stream) -> dict:
+    """Per-call device time of ``calls`` consecutive steps, each bracketed by
+    its own pair of HIP events on the launch stream."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(calls)]
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(evs):
+        a.record(stream)
+        step(i)
+        b.record(stream)
+    torch.cuda.synchronize()
+    us = sorted(a.elapsed_time(b) * 1000.0 for a, b in evs)
+
+    def pct(q):
+        return round(us[min(len(us) - 1, int(q * len(us)))], 2)
+
+    return {"p50_us": pct(0.50), "p99_us": pct(0.99), "min_us": round(us[0], 2), "max_us": round(us[-1], 2),
+            "calls": calls}
+
+
+def graph_timing(step, nrot: int, steps: int, warmup: int, dev) -> dict:
+    """The same steps captured into one HIP graph (one captured call per input
+    copy, replayed until ``steps`` calls have run), timed with HIP events."""
+    import torch
+    per = max(nrot, 32)
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        for i in range(per):        # eager warm-up on the capture stream
+            step(i)
+    torch.cuda.current_stream(dev).wait_stream(side)
+    torch.cuda.synchronize(dev)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        for i in range(per):
+            step(i)
+    torch.cuda.synchronize(dev)
+    reps = max(1, steps // per)
+    for _ in range(max(1, warmup // per)):
+        g.replay()
+    stream = torch.cuda.current_stream(dev)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    ev0.record(stream)
+    for _ in range(reps):
+        g.replay()
+    ev1.record(stream)
+    torch.cuda.synchronize(dev)
+    ms = ev0.elapsed_time(ev1) / (reps * per)
+    return {"value": round(1000.0 / ms, 1), "unit": "verify-steps/s", "ms_per_step": round(ms, 6),
+            "steps": reps * per, "what": f"{per} calls captured into one HIP graph, replayed {reps} times"}
 
 
 def unfused_baseline(w, sets, tok, uni, steps: int, warmup: int):
@@ -143,6 +261,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true", help="skip timing the unfused PyTorch comparison")
+    ap.add_argument("--graph", choices=("auto", "on", "off"), default="auto",
+                    help="also time the calls replayed from a HIP graph (auto: for workloads under 8 MB)")
     ap.add_argument("--copy-calibration-mb", type=float, default=0.0,
                     help="only run a plain copy of this size (for counter calibration) and exit")
     args = ap.parse_args()
@@ -155,22 +275,33 @@ def main() -> int:
         copy_calibration(int(args.copy_calibration_mb * 1e6), 20)
         return 0
 
+    from paper_2406_11016_amd import workloads as W
+
+    w = W.WORKLOADS[args.workload or W.HEADLINE]
+    log(f"generating {w.name} ({w.logit_bytes / 1e6:.1f} MB of logits)")
+    t0 = time.perf_counter()
+    x = W.generate(w)
+    log(f"generated in {time.perf_counter() - t0:.1f} s")
+
+    # the CPU leg runs first: its process pool forks, which must happen
+    # before this process initialises the GPU
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"timing the CPU oracle: one thread, then a process pool, ~{args.cpu_seconds:.0f} s each")
+        cpu = cpu_baseline(w, x, args.cpu_seconds)
+        log(f"CPU oracle: {cpu['single_thread']['value']:.4f} steps/s on one thread, "
+            f"{cpu['value']:.4f} steps/s on {cpu['cores']} processes")
+
     import torch
 
     from paper_2406_11016_amd import binding
-    from paper_2406_11016_amd import workloads as W
 
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         return 1
-    w = W.WORKLOADS[args.workload or W.HEADLINE]
     dev = torch.device("cuda:0")
     binding.load_library()
-
-    log(f"generating {w.name} ({w.logit_bytes / 1e6:.1f} MB of logits)")
-    t0 = time.perf_counter()
-    x = W.generate(w)
-    log(f"generated in {time.perf_counter() - t0:.1f} s; uploading")
+    log("uploading")
     d0, t0_, tok, uni = binding.to_device(x, dev)
     nrot = max(1, int((args.rotate_mb * 1e6 + w.logit_bytes - 1) // w.logit_bytes))
     sets = [(d0, t0_)] + [(d0.clone(), t0_.clone()) for _ in range(nrot - 1)]
@@ -206,6 +337,15 @@ def main() -> int:
     steps_per_s = 1000.0 / ms_per_step
     log(f"{ms_per_step * 1000:.2f} us/step (events), wall {wall:.3f} s")
 
+    ncalls = min(max(args.steps, 50), 1000)
+    log(f"per-call latency over {ncalls} calls")
+    latency = latency_percentiles(step, ncalls, stream)
+
+    graph = None
+    if args.graph == "on" or (args.graph == "auto" and w.logit_bytes < 8e6):
+        log("timing the same calls replayed from a HIP graph")
+        graph = graph_timing(step, nrot, args.steps, args.warmup, dev)
+
     # the decisions of the timed steps are real: check one against the oracle
     # later in the tests; here just make sure they are in range
     a, n = acc.cpu(), nxt.cpu()
@@ -225,11 +365,6 @@ def main() -> int:
         unfused = unfused_baseline(w, sets, tok, uni, steps=max(20, min(200, args.steps // 10)), warmup=5)
         unfused["speedup_of_fused"] = round(steps_per_s / unfused["value"], 2)
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        log(f"timing the CPU oracle for ~{args.cpu_seconds:.0f} s")
-        cpu = cpu_baseline(w, x, args.cpu_seconds)
-
     out = {
         "metric": METRIC, "value": round(steps_per_s, 1), "unit": "verify-steps/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 6),
@@ -238,6 +373,8 @@ def main() -> int:
         "config": {"workload": w.name, "mode": w.mode, "batch": w.batch, "gamma": w.gamma, "vocab": w.vocab,
                    "logits": w.dtype, "temperature": w.temperature, "rotating_copies": nrot},
         "roofline": roofline,
+        "latency": latency,
+        "graph": graph,
         "cpu_baseline": cpu,
         "unfused_torch": unfused,
     }
