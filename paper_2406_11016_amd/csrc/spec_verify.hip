@@ -531,7 +531,7 @@ struct Smem {
     int result, cross;
     float kmax;
     unsigned long long flags[kWaves][3];
-    double cross_t;
+    double cross_t, cross_tot;
 };
 
 // Stats slots of a batch element: the rows its decision reads first (target
@@ -618,38 +618,31 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot,
 }
 
 // Row log2-normalisers Lambda = Kmax + log2(sum S 2^(K - Kmax)) of R rows
-// from the (K, S) pairs of their W sub-chunks in LDS, into sm.rowL:
-// one thread per row, in sub-chunk order, reading blocks of 16 pairs at a time
-// (clamped, masked indices) so each block costs one LDS round trip.  Ends
-// with a workgroup barrier.
+// from the (K, S) pairs of their W sub-chunks in LDS, into sm.rowL: row i
+// belongs to an aligned group of G lanes (the largest power of two <= 16 with
+// R G <= kThreads, rows beyond kThreads in further rounds); lane g of the
+// group takes pairs g, g + G, ... in order, and a DPP butterfly combines the
+// group in a fixed order, so equal rows give equal bits.  The group's first
+// lane takes the logarithm.  Ends with a workgroup barrier.
 __device__ __forceinline__ void merge_rows(Smem& sm, int R, int W) {
-    constexpr int U = 16;
-    for (int i = threadIdx.x; i < R; i += kThreads) {
+    const int G = (R <= 16) ? 16 : (R <= 32) ? 8 : (R <= 64) ? 4 : (R <= 128) ? 2 : 1;
+    const int g = threadIdx.x % G;
+    for (int i0 = 0; i0 < R; i0 += kThreads / G) {
+        const int i = i0 + (int)threadIdx.x / G;
+        const bool row = i < R;
         const float* K = sm.K + (size_t)i * W;
         const double* S = sm.S + (size_t)i * W;
         float m = -INFINITY;
-        for (int j0 = 0; j0 < W; j0 += U) {
-            float k[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) k[u] = K[min(j0 + u, W - 1)];
-#pragma unroll
-            for (int u = 0; u < U; ++u) m = fmaxf(m, k[u]);  // repeats of the last pair change nothing
-        }
+        if (row)
+            for (int j = g; j < W; j += G) m = fmaxf(m, K[j]);
+        m = group_max(m, G);
         double sum = 0.0;
-        for (int j0 = 0; j0 < W; j0 += U) {
-            float k[U];
-            double t[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                k[u] = K[min(j0 + u, W - 1)];
-                t[u] = S[min(j0 + u, W - 1)];
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (j0 + u < W) sum += ldexp(t[u], exp_delta(k[u] - m));
-        }
+        if (row)
+            for (int j = g; j < W; j += G) sum += ldexp(S[j], exp_delta(K[j] - m));
+        sum = group_sum(sum, G);
         // a NaN logit makes S NaN; a +inf logit makes K +inf and S NaN
-        sm.rowL[i] = (sum != sum) ? __builtin_nan("") : ((m == -INFINITY) ? -INFINITY : (double)m + log2(sum));
+        if (row && g == 0)
+            sm.rowL[i] = (sum != sum) ? __builtin_nan("") : ((m == -INFINITY) ? -INFINITY : (double)m + log2(sum));
     }
     __syncthreads();
 }
@@ -868,6 +861,30 @@ __device__ __forceinline__ int mass_locate(const double* m, int M, double t, con
     return sm.cross;
 }
 
+// Inverse-CDF locate over at most kWave masses by one wave (all its lanes
+// call this; lane l holds mass l, 0 beyond the last): sm.cross receives the
+// first mass at which the running sum exceeds t = u * total -- or the last
+// positive mass, if rounding leaves t at or beyond the total; -1 if no mass
+// is positive -- sm.cross_t the part of t inside it and sm.cross_tot the
+// total.  The caller's barrier publishes them.
+__device__ __forceinline__ void wave_locate(double m, double u, Smem& sm) {
+    const int lane = threadIdx.x % kWave;
+    const double incl = wave_inclusive_scan(m);
+    const double tot = lane_f64(incl, kWave - 1);
+    const double t = u * tot;
+    const unsigned long long over = __ballot(incl > t && m > 0.0);
+    const unsigned long long pos = __ballot(m > 0.0);
+    const int j = over ? __ffsll((long long)over) - 1 : (pos ? 63 - __clzll((long long)pos) : -1);
+    const int jc = max(j, 0);
+    const double before = lane_f64(incl, max(jc - 1, 0));
+    const double mj = lane_f64(m, jc);
+    if (lane == 0) {
+        sm.cross_tot = tot;
+        sm.cross = j;
+        sm.cross_t = over ? t - ((jc == 0) ? 0.0 : before) : mj;
+    }
+}
+
 // b's decision, made once by b's decider workgroup and published as a small
 // record, one copy per reader (each mass workgroup, the draw, the bonus
 // workgroup), which that reader clears once it has read it.  The decider also
@@ -985,32 +1002,12 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
             const float K = (tid < W) ? sm.K[tid] : -INFINITY;
             const double S = (tid < W) ? sm.S[tid] : 0.0;
             const float m0 = wave_max(K);
-            const double m = ldexp(S, exp_delta(K - m0));
-            double incl = m;
-#pragma unroll
-            for (int o = 1; o < kWave; o <<= 1) {
-                const double nb = __shfl_up(incl, o, kWave);
-                if (tid >= o) incl += nb;
-            }
-            const double up1 = __shfl_up(incl, 1, kWave);  // every lane takes part in the shuffle
-            const double excl = (tid == 0) ? 0.0 : up1;
-            const double tot = __shfl(incl, kWave - 1, kWave);
-            const double t = u * tot;
-            const unsigned long long over = __ballot(incl > t && m > 0.0);
-            const unsigned long long pos = __ballot(m > 0.0);
-            // first chunk whose running sum exceeds t; if rounding leaves t at
-            // or beyond the total, the last chunk with mass
-            const int jj = over ? __ffsll((long long)over) - 1 : (pos ? 63 - __clzll((long long)pos) : -1);
-            if (tid == 0) {
-                sm.kmax = m0;
-                sm.scratch[0] = tot;
-                sm.cross = jj;
-            }
-            if (jj >= 0 && tid == jj) sm.cross_t = over ? t - excl : m;
+            if (tid == 0) sm.kmax = m0;
+            wave_locate(ldexp(S, exp_delta(K - m0)), u, sm);
         }
         __syncthreads();
         km = sm.kmax;
-        total = sm.scratch[0];
+        total = sm.cross_tot;
         j = sm.cross;
         t_local = sm.cross_t;
     } else {
@@ -1114,8 +1111,20 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
     int idx = -1;
     double total = __builtin_nan("");
     for (int pass = 0; pass < 2 && !bad; ++pass) {
-        double loc[4];
-        total = mass_prefix(sm.sub, M, sm, loc);
+        // the mass the uniform falls in: one wave when there are at most 64
+        double t_local = 0.0;
+        int j = -1;
+        if (M <= kWave) {
+            if (tid < kWave) wave_locate((tid < M) ? sm.sub[tid] : 0.0, u, sm);
+            __syncthreads();
+            total = sm.cross_tot;
+            j = sm.cross;
+            t_local = sm.cross_t;
+        } else {
+            double loc[4];
+            total = mass_prefix(sm.sub, M, sm, loc);
+            if (isfinite(total) && total > 0.0) j = mass_locate(sm.sub, M, u * total, loc, sm, &t_local);
+        }
         if (!(isfinite(total) && total >= 0.0)) {
             bad = true;
             break;
@@ -1140,8 +1149,6 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
             bad = true;
             break;
         }
-        double t_local = 0.0;
-        const int j = mass_locate(sm.sub, M, u * total, loc, sm, &t_local);
         if (j < 0) {
             bad = true;
             break;

@@ -124,6 +124,9 @@ constexpr int kDppSwap1 = 0xB1;        // quad_perm [1, 0, 3, 2]
 constexpr int kDppSwap2 = 0x4E;        // quad_perm [2, 3, 0, 1]
 constexpr int kDppHalfMirror = 0x141;  // lane i <- 7 - i within each half row
 constexpr int kDppMirror = 0x140;      // lane i <- 15 - i within each row
+constexpr int kDppRowShr = 0x110;      // + n: lane i <- i - n within each row
+constexpr int kDppRowBcast15 = 0x142;  // lane 15 of each row -> the next row
+constexpr int kDppRowBcast31 = 0x143;  // lane 31 -> rows 2 and 3
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_f32(float v) {
@@ -135,6 +138,16 @@ __device__ __forceinline__ double dpp_f64(double v) {
     const long long x = __double_as_longlong(v);
     const int lo = __builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
     const int hi = __builtin_amdgcn_update_dpp(0, (int)(x >> 32), CTRL, 0xF, 0xF, false);
+    return __longlong_as_double(((long long)hi << 32) | (long long)(unsigned int)lo);
+}
+
+// A DPP move of a double into the rows ROWS; lanes with no source in range,
+// or outside ROWS, read 0.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_f64_or0(double v) {
+    const long long x = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(x >> 32), CTRL, ROWS, 0xF, false);
     return __longlong_as_double(((long long)hi << 32) | (long long)(unsigned int)lo);
 }
 
@@ -165,6 +178,38 @@ __device__ __forceinline__ double wave_sum(double v) {
     return (lane_f64(v, 0) + lane_f64(v, 16)) + (lane_f64(v, 32) + lane_f64(v, 48));
 }
 
+// Inclusive prefix sums over the wave in lane order (fixed order, fp64):
+// shifts by 1, 2, 4 and 8 within each 16-lane row, then row 0's total into
+// row 1 and row 2's into row 3, then the total of rows 0-1 into rows 2-3.
+__device__ __forceinline__ double wave_inclusive_scan(double v) {
+    v += dpp_f64_or0<kDppRowShr + 1, 0xF>(v);
+    v += dpp_f64_or0<kDppRowShr + 2, 0xF>(v);
+    v += dpp_f64_or0<kDppRowShr + 4, 0xF>(v);
+    v += dpp_f64_or0<kDppRowShr + 8, 0xF>(v);
+    v += dpp_f64_or0<kDppRowBcast15, 0xA>(v);
+    v += dpp_f64_or0<kDppRowBcast31, 0xC>(v);
+    return v;
+}
+
+// Maximum / sum over aligned groups of G (1, 2, 4, 8 or 16) lanes, left in
+// every lane of the group; the same butterfly as wave_max / wave_sum, cut
+// after log2(G) steps.  G must be uniform over the wave.
+__device__ __forceinline__ float group_max(float v, int G) {
+    if (G >= 2) v = fmaxf(v, dpp_f32<kDppSwap1>(v));
+    if (G >= 4) v = fmaxf(v, dpp_f32<kDppSwap2>(v));
+    if (G >= 8) v = fmaxf(v, dpp_f32<kDppHalfMirror>(v));
+    if (G >= 16) v = fmaxf(v, dpp_f32<kDppMirror>(v));
+    return v;
+}
+
+__device__ __forceinline__ double group_sum(double v, int G) {
+    if (G >= 2) v += dpp_f64<kDppSwap1>(v);
+    if (G >= 4) v += dpp_f64<kDppSwap2>(v);
+    if (G >= 8) v += dpp_f64<kDppHalfMirror>(v);
+    if (G >= 16) v += dpp_f64<kDppMirror>(v);
+    return v;
+}
+
 __device__ __forceinline__ int wave_max_int(int v) {
 #pragma unroll
     for (int o = kWave / 2; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, kWave));
@@ -191,11 +236,7 @@ __device__ __forceinline__ double block_inclusive_scan(double v, double* scratch
                                                        double* total) {
     const int wave = threadIdx.x / kWave;
     const int lane = threadIdx.x % kWave;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const double n = __shfl_up(v, o, kWave);
-        if (lane >= o) v += n;
-    }
+    v = wave_inclusive_scan(v);
     __syncthreads();
     if (lane == kWave - 1) scratch[wave] = v;
     __syncthreads();

@@ -70,6 +70,17 @@ def test_vocab_edge_sizes(dtype, V):
         compare(x, run_gpu(x), run_oracle(x), label=f"V={V} {dtype} g={gamma}")
 
 
+@pytest.mark.parametrize("gamma", [1, 2, 5, 13, 16, 17, 20, 31, 33, 64, 65, 100, 128])
+def test_gamma_range(gamma):
+    # the row-normaliser merge groups 16, 8, 4, 2 or 1 lanes per row by the
+    # number of rows (2 gamma); low noise so that long accepted prefixes occur
+    for dtype, V, mode in (("f32", 3001, "exact"), ("bf16", 20011, "exact"), ("f16", 5003, "sigmoid")):
+        x = W.small_case(3, gamma, V, dtype, mode=mode, seed=200 + gamma, noise_scale=0.05,
+                         alpha=-1e3, beta=1e3)
+        nflag = compare(x, run_gpu(x), run_oracle(x), label=f"gamma={gamma} {dtype} {mode}")
+        _report(f"gamma={gamma}", x, nflag)
+
+
 @pytest.mark.parametrize("mode", ["exact", "sigmoid"])
 def test_unaligned_rows_and_offsets(mode):
     # odd V in fp32: every row after the first starts off a 16-byte boundary
