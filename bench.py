@@ -263,6 +263,10 @@ def main() -> int:
     ap.add_argument("--no-unfused", action="store_true", help="skip timing the unfused PyTorch comparison")
     ap.add_argument("--graph", choices=("auto", "on", "off"), default="auto",
                     help="also time the calls replayed from a HIP graph (auto: for workloads under 8 MB)")
+    ap.add_argument("--sweep", choices=("gamma", "alpha_beta", "decode_loop"), default=None,
+                    help="instead of the benchmark line: one JSON line with a sweep over gamma (1..20), over "
+                         "the sigmoid constants alpha = -beta, or the decoding loop with the gamma rule "
+                         "(--steps iterations)")
     ap.add_argument("--copy-calibration-mb", type=float, default=0.0,
                     help="only run a plain copy of this size (for counter calibration) and exit")
     args = ap.parse_args()
@@ -274,6 +278,9 @@ def main() -> int:
     if args.copy_calibration_mb > 0:
         copy_calibration(int(args.copy_calibration_mb * 1e6), 20)
         return 0
+    if args.sweep is not None:
+        import bench_sweeps
+        return bench_sweeps.run(args.sweep, args.steps, args.warmup)
 
     from paper_2406_11016_amd import workloads as W
 

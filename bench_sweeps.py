@@ -1,0 +1,218 @@
+"""Parameter sweeps of the fused verification step on one GPU (``bench.py --sweep``).
+
+* ``gamma``: the number of drafted tokens, 1 .. 20 (the paper sweeps gamma in
+  Sec. 4.3 and Fig. 3), on B = 1 workloads shaped like the paper's ASR
+  (V = 51,865, fp32 logits) and summarisation (V = 32,000, fp16 logits) runs,
+  and on the batched bf16 workload (B = 64, V = 128,256) at a few gamma.  Per
+  point: time per step, verify-steps/s, the fraction of 8 TB/s on the
+  algorithmic bytes, and, from a batch of 32 independent elements of the same
+  value law, the acceptance rate (mean accepted length / gamma), the chance
+  that every draft is accepted and the tokens emitted per step (L + 1).
+* ``alpha_beta``: the sigmoid approximation's constants alpha = -beta in
+  {10, 1e3, 1e4, 1e5} (Sec. 3.2, eq. (5); Tables 2, 7, 8) on the fp16 sigmoid
+  workload (B = 32, gamma = 10, V = 50,272, T = 0.7).  The exact mode runs on
+  the same inputs and uniforms.  Per point: time per step; acceptance rate of
+  both modes and its change; token disagreement rate; mean total-variation
+  distance between the two final-token distributions where both modes select
+  the same row; and the number of sentinel or non-finite outputs (fp16
+  logits scaled by 1/(beta - alpha) stay finite in the fp32 arithmetic).
+
+Every statistic comes from the GPU path's own outputs (its probe buffers for
+the distributions).  Inputs are the seeded synthetic workloads.
+"""
+from __future__ import annotations
+
+import json
+import sys
+import time
+
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(msg: str) -> None:
+    print(f"[sweep] {msg}", file=sys.stderr, flush=True)
+
+
+def _time_steps(w, x, steps: int, warmup: int, rotate_mb: float = 768.0) -> float:
+    """Microseconds per call, HIP events on the launch stream, rotating input copies."""
+    import torch
+
+    from paper_2406_11016_amd import binding
+    dev = torch.device("cuda:0")
+    d0, t0, tok, uni = binding.to_device(x, dev)
+    nrot = max(1, int((rotate_mb * 1e6 + w.logit_bytes - 1) // w.logit_bytes))
+    sets = [(d0, t0)] + [(d0.clone(), t0.clone()) for _ in range(nrot - 1)]
+    acc = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    nxt = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    ws = binding.new_workspace(w.batch, w.gamma, w.vocab, d0.dtype, dev)
+
+    def step(i):
+        d, t = sets[i % nrot]
+        binding.verify(d, t, tok, uni, mode=w.mode, temperature=w.temperature, alpha=w.alpha, beta=w.beta,
+                       accepted_len=acc, next_token=nxt, workspace=ws)
+
+    for i in range(warmup):
+        step(i)
+    stream = torch.cuda.current_stream(dev)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    ev0.record(stream)
+    for i in range(steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize(dev)
+    us = ev0.elapsed_time(ev1) / steps * 1000.0
+    del sets, d0, t0, ws
+    torch.cuda.empty_cache()
+    return us
+
+
+def _acceptance(w, batch: int, seed: int):
+    """Accepted lengths of `batch` independent elements of the workload's law."""
+    import torch
+
+    from paper_2406_11016_amd import binding
+    from paper_2406_11016_amd import workloads as W
+    x = W.generate(w.with_(batch=batch), seed=seed)
+    d, t, tok, uni = binding.to_device(x, "cuda")
+    acc, nxt = binding.verify(d, t, tok, uni, mode=w.mode, temperature=w.temperature, alpha=w.alpha,
+                              beta=w.beta)
+    torch.cuda.synchronize()
+    return acc.cpu().numpy(), nxt.cpu().numpy()
+
+
+def sweep_gamma(steps: int, warmup: int) -> dict:
+    import numpy as np
+
+    from bench import algorithmic_bytes
+    from paper_2406_11016_amd import workloads as W
+    plan = [("exact_b1_g5_v51865_f32", list(range(1, 21))),
+            ("exact_b1_g10_v32000_f16", list(range(1, 21))),
+            ("exact_b64_g8_v128256_bf16", [1, 2, 4, 8, 12, 16, 20])]
+    points = []
+    for base, gammas in plan:
+        for g in gammas:
+            w = W.WORKLOADS[base].with_(gamma=g)
+            x = W.generate(w)
+            n = steps if w.batch == 1 else max(50, steps // 5)
+            us = _time_steps(w, x, n, warmup)
+            del x
+            L, _ = _acceptance(w, 32 if w.batch == 1 else 16, seed=w.seed * 1000 + g)
+            valid = L >= 0
+            Lv = L[valid].astype(np.float64)
+            alg = algorithmic_bytes(w)
+            p = {"workload": base, "gamma": g, "batch": w.batch, "vocab": w.vocab, "logits": w.dtype,
+                 "us_per_step": round(us, 3), "steps_per_s": round(1e6 / us, 1),
+                 "frac_of_8TBs": round(alg / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                 "accept_rate": round(float(Lv.mean() / g), 4),
+                 "p_all_accepted": round(float((Lv == g).mean()), 4),
+                 "tokens_per_step": round(float(Lv.mean() + 1.0), 3),
+                 "us_per_token_per_element": round(us / float(Lv.mean() + 1.0) / w.batch, 3),
+                 "sentinels": int((~valid).sum()), "acceptance_sample": int(L.size)}
+            log(json.dumps(p))
+            points.append(p)
+    return {"sweep": "gamma", "points": points}
+
+
+def sweep_alpha_beta(steps: int, warmup: int) -> dict:
+    import numpy as np
+    import torch
+
+    from paper_2406_11016_amd import binding
+    from paper_2406_11016_amd import workloads as W
+    base = W.WORKLOADS["sigmoid_b32_g10_v50272_f16_t0.7"]
+    sets = [W.generate(base, seed=base.seed * 100 + k) for k in range(4)]
+    points = []
+
+    def run(x, mode, a, b):
+        d, t, tok, uni = binding.to_device(x, "cuda")
+        acc, nxt, pr = binding.verify(d, t, tok, uni, mode=mode, temperature=x.temperature, alpha=a, beta=b,
+                                      probe=True)
+        torch.cuda.synchronize()
+        return acc.cpu().numpy(), nxt.cpu().numpy(), pr.weights, pr.mass
+
+    exact = [run(x, "exact", -1.0, 1.0) for x in sets]
+    for ab in (10.0, 1e3, 1e4, 1e5):
+        w = base.with_(alpha=-ab, beta=ab)
+        us = _time_steps(w, sets[0], steps, warmup)
+        Ls, Le, dis, tvs, bad = [], [], [], [], 0
+        for x, (le, ne, we, me) in zip(sets, exact):
+            ls, ns, wsg, ms = run(x, "sigmoid", -ab, ab)
+            bad += int((ls < 0).sum() + (ns < 0).sum())
+            bad += int((~torch.isfinite(ms)).sum().item())
+            Ls.append(ls)
+            Le.append(le)
+            dis.append((ls != le) | (ns != ne))
+            same = torch.from_numpy((ls == le) & (ls >= 0)).to(wsg.device)
+            if bool(same.any()):
+                ps = wsg[same].double() / ms[same][:, None]
+                pe = we[same].double() / me[same][:, None]
+                tvs.append((0.5 * (ps - pe).abs().sum(dim=1)).cpu().numpy())
+        Ls, Le = np.concatenate(Ls), np.concatenate(Le)
+        g = base.gamma
+        p = {"alpha": -ab, "beta": ab, "us_per_step": round(us, 3), "steps_per_s": round(1e6 / us, 1),
+             "accept_rate_sigmoid": round(float(Ls[Ls >= 0].mean() / g), 5),
+             "accept_rate_exact": round(float(Le[Le >= 0].mean() / g), 5),
+             "token_disagreement": round(float(np.concatenate(dis).mean()), 4),
+             "mean_tv_same_row": round(float(np.concatenate(tvs).mean()), 4) if tvs else None,
+             "sentinel_or_nonfinite": bad, "elements": int(Ls.size)}
+        p["accept_delta"] = round(p["accept_rate_sigmoid"] - p["accept_rate_exact"], 5)
+        log(json.dumps(p))
+        points.append(p)
+    return {"sweep": "alpha_beta", "workload": base.name, "points": points}
+
+
+def decode_loop(iterations: int, gamma_max: int = 20, pool: int = 32) -> dict:
+    """The decoding loop (gamma rule, one captured graph per gamma) on the B = 1
+    workloads, against the same loop with eager calls."""
+    import numpy as np
+
+    from paper_2406_11016_amd import workloads as W
+    from paper_2406_11016_amd.decode_loop import DecodeLoop, SyntheticSteps
+    runs = []
+    for name in ("exact_b1_g5_v51865_f32", "exact_b1_g10_v32000_f16"):
+        w = W.WORKLOADS[name]
+        src = SyntheticSteps(w, gamma_max=gamma_max, pool=pool)
+        for graphs in (True, False):
+            loop = DecodeLoop(w.batch, w.vocab, w.dtype, mode=w.mode, temperature=w.temperature, alpha=w.alpha,
+                              beta=w.beta, gamma0=5, gamma_max=gamma_max, use_graphs=graphs)
+            if graphs:
+                loop.capture_all()
+            loop.run(src, 20)                                   # warm-up
+            t0 = time.perf_counter()
+            st = loop.run(src, iterations)
+            wall = time.perf_counter() - t0
+            dev = loop.run(src, min(iterations, 500), time_device=True).device_us
+            gam = np.array(st.gammas)
+            p = {"workload": name, "graphs": graphs, "iterations": iterations,
+                 "us_per_iteration": round(wall / iterations * 1e6, 2),
+                 "tokens_per_iteration": round(st.tokens / iterations / w.batch, 3),
+                 "tokens_per_s": round(st.tokens / wall, 1),
+                 "mean_gamma": round(float(gam.mean()), 2),
+                 "gamma_histogram": {int(k): int(v) for k, v in zip(*np.unique(gam, return_counts=True))},
+                 "step_device_us_p50": round(float(np.percentile(dev, 50)), 2),
+                 "step_device_us_p99": round(float(np.percentile(dev, 99)), 2)}
+            log(json.dumps(p))
+            runs.append(p)
+    return {"sweep": "decode_loop", "gamma0": 5, "gamma_max": gamma_max, "runs": runs,
+            "what": "iterations of: copy the next synthetic step's logits into the loop's static buffers, "
+                    "verify, copy L and the next token to pinned host memory, synchronise, apply the gamma rule"}
+
+
+def run(kind: str, steps: int, warmup: int) -> int:
+    import torch
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        return 1
+    from paper_2406_11016_amd import binding
+    binding.load_library()
+    t0 = time.perf_counter()
+    if kind == "gamma":
+        out = sweep_gamma(steps, warmup)
+    elif kind == "alpha_beta":
+        out = sweep_alpha_beta(steps, warmup)
+    else:
+        out = decode_loop(steps)
+    out["seconds"] = round(time.perf_counter() - t0, 1)
+    print(json.dumps(out), flush=True)
+    return 0

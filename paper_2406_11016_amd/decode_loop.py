@@ -1,0 +1,196 @@
+"""A multi-step decoding loop around the fused verification step.
+
+Each iteration verifies gamma drafted tokens per batch element with one call
+of the step and then sets gamma for the next iteration with the draft-length
+rule the paper's experiments use (Sec. 4, hyperparameters; the rule of the
+assisted-generation baseline it compares with): gamma starts at 5, grows by 2
+after an iteration in which every drafted token was accepted and otherwise
+shrinks by 1.  Readings where the paper is silent: gamma never drops below 1
+nor exceeds ``gamma_max``, and with several batch elements "every drafted
+token accepted" must hold for all of them.
+
+The loop owns static device buffers sized for ``gamma_max``.  Whatever
+produces the logits (the draft and target models of a decoder; a synthetic
+source here) writes an iteration's ``[B, gamma, V]`` / ``[B, gamma + 1, V]``
+logits, drafted tokens and uniforms into the leading part of those buffers,
+and the call for each gamma is captured once into a HIP graph (lazily, on
+first use) and replayed, so an iteration costs one graph launch, two small
+device-to-host copies into pinned memory and one stream synchronisation --
+the host needs the accepted length to decide the next gamma and which tokens
+to append.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+import torch
+
+from . import binding
+from .binding import STORAGE_TORCH_DTYPES
+
+
+def next_gamma(gamma: int, accepted: np.ndarray, gamma_max: int, grow: int = 2, shrink: int = 1) -> int:
+    """The draft-length rule: ``gamma + grow`` (at most ``gamma_max``) if every
+    element accepted all ``gamma`` drafts, else ``gamma - shrink`` (at least 1).
+    Elements with the sentinel (-1) count as not accepted."""
+    if accepted.size > 0 and bool(np.all(accepted == gamma)):
+        return min(gamma + grow, gamma_max)
+    return max(gamma - shrink, 1)
+
+
+@dataclass
+class LoopStats:
+    iterations: int = 0
+    tokens: int = 0                                   # accepted drafts + 1 per element and iteration
+    gammas: List[int] = field(default_factory=list)
+    accepted: List[np.ndarray] = field(default_factory=list)
+    next_tokens: List[np.ndarray] = field(default_factory=list)
+    device_us: List[float] = field(default_factory=list)   # per iteration, when timed
+
+
+class DecodeLoop:
+    """Static buffers, one captured graph per gamma, and the gamma rule."""
+
+    def __init__(self, batch: int, vocab: int, dtype: str, *, mode: str = "exact", temperature: float = 1.0,
+                 alpha: float = -1.0e4, beta: float = 1.0e4, gamma0: int = 5, gamma_max: int = 20,
+                 use_graphs: bool = True, device="cuda"):
+        if not (1 <= gamma0 <= gamma_max):
+            raise ValueError("need 1 <= gamma0 <= gamma_max")
+        self.B, self.V, self.dtype, self.mode = batch, vocab, dtype, mode
+        self.temperature, self.alpha, self.beta = temperature, alpha, beta
+        self.gamma0, self.gamma_max, self.use_graphs = gamma0, gamma_max, use_graphs
+        self.device = torch.device(device)
+        tdt = STORAGE_TORCH_DTYPES[dtype]
+        B, G, V = batch, gamma_max, vocab
+        self.draft = torch.empty(B * G * V, dtype=tdt, device=self.device)
+        self.target = torch.empty(B * (G + 1) * V, dtype=tdt, device=self.device)
+        self.tokens = torch.zeros(B * G, dtype=torch.int32, device=self.device)
+        self.uniforms = torch.zeros(B * (G + 1), dtype=torch.float32, device=self.device)
+        self.acc = torch.empty(B, dtype=torch.int32, device=self.device)
+        self.nxt = torch.empty(B, dtype=torch.int32, device=self.device)
+        self.host = torch.empty(2 * B, dtype=torch.int32, pin_memory=True)
+        ws = max(binding.workspace_bytes(B, g, V, tdt) for g in range(1, G + 1))
+        self.ws = torch.zeros((ws + 15) // 16 * 16, dtype=torch.uint8, device=self.device)
+        self.stream = torch.cuda.Stream(self.device)
+        self.graphs: Dict[int, torch.cuda.CUDAGraph] = {}
+
+    # -- the buffers an iteration's producer writes ---------------------------
+    def views(self, gamma: int) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
+        """Contiguous ``draft [B, gamma, V]``, ``target [B, gamma + 1, V]``,
+        ``tokens [B, gamma]``, ``uniforms [B, gamma + 1]`` on the static buffers."""
+        if not (1 <= gamma <= self.gamma_max):
+            raise ValueError(f"gamma {gamma} outside 1 .. {self.gamma_max}")
+        B, V = self.B, self.V
+        return (self.draft[:B * gamma * V].view(B, gamma, V), self.target[:B * (gamma + 1) * V].view(B, gamma + 1, V),
+                self.tokens[:B * gamma].view(B, gamma), self.uniforms[:B * (gamma + 1)].view(B, gamma + 1))
+
+    def _call(self, gamma: int) -> None:
+        d, t, tok, u = self.views(gamma)
+        binding.verify(d, t, tok, u, mode=self.mode, temperature=self.temperature, alpha=self.alpha,
+                       beta=self.beta, accepted_len=self.acc, next_token=self.nxt, workspace=self.ws)
+
+    def _graph(self, gamma: int) -> torch.cuda.CUDAGraph:
+        g = self.graphs.get(gamma)
+        if g is None:
+            with torch.cuda.stream(self.stream):
+                self._call(gamma)          # eager once on the capture stream (checks the arguments)
+            self.stream.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=self.stream):
+                self._call(gamma)
+            self.stream.synchronize()
+            self.graphs[gamma] = g
+        return g
+
+    def capture_all(self) -> None:
+        """Capture every gamma up front (keeps capture out of a timed loop)."""
+        for g in range(1, self.gamma_max + 1):
+            self._graph(g)
+
+    # -- one iteration ---------------------------------------------------------
+    def launch(self, gamma: int) -> None:
+        """Enqueue the verification of the buffers' current contents on the loop's stream."""
+        if self.use_graphs:
+            graph = self._graph(gamma)
+            with torch.cuda.stream(self.stream):
+                graph.replay()
+        else:
+            with torch.cuda.stream(self.stream):
+                self._call(gamma)
+
+    def collect(self) -> Tuple[np.ndarray, np.ndarray]:
+        """Wait for the launched call; its accepted lengths and next tokens."""
+        B = self.B
+        with torch.cuda.stream(self.stream):
+            self.host[:B].copy_(self.acc, non_blocking=True)
+            self.host[B:].copy_(self.nxt, non_blocking=True)
+        self.stream.synchronize()
+        h = self.host.numpy()
+        return h[:B].copy(), h[B:].copy()
+
+    def run(self, producer, iterations: int, stats: Optional[LoopStats] = None,
+            time_device: bool = False) -> LoopStats:
+        """``iterations`` rounds of: producer(self, i, gamma) fills the buffers
+        (on ``self.stream``), the step runs, gamma is updated.  With
+        ``time_device`` each step is bracketed by HIP events on the stream."""
+        stats = stats or LoopStats()
+        gamma = self.gamma0
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) if time_device else None
+        for i in range(iterations):
+            producer(self, i, gamma)
+            if ev is not None:
+                ev[0].record(self.stream)
+            self.launch(gamma)
+            if ev is not None:
+                ev[1].record(self.stream)
+            L, nx = self.collect()
+            if ev is not None:
+                stats.device_us.append(ev[0].elapsed_time(ev[1]) * 1000.0)
+            stats.iterations += 1
+            stats.gammas.append(gamma)
+            stats.accepted.append(L)
+            stats.next_tokens.append(nx)
+            stats.tokens += int(np.sum(np.where(L >= 0, L + 1, 0)))
+            gamma = next_gamma(gamma, L, self.gamma_max)
+        return stats
+
+
+class SyntheticSteps:
+    """A device-resident pool of synthetic verification inputs at ``gamma_max``
+    drafts; iteration i uses entry ``i % len(pool)``, cut to the iteration's
+    gamma (rows are drawn independently, so the first gamma drafts of an
+    entry are a valid gamma-draft)."""
+
+    def __init__(self, workload, gamma_max: int, pool: int, device="cuda", seed0: Optional[int] = None):
+        from . import workloads as W
+        self.inputs = []
+        self.dev = []
+        base = workload.with_(gamma=gamma_max)
+        for k in range(pool):
+            x = W.generate(base, seed=(seed0 if seed0 is not None else base.seed * 1000) + k)
+            self.inputs.append(x)
+            self.dev.append(binding.to_device(x, device))
+        torch.cuda.synchronize(device)
+
+    def __len__(self) -> int:
+        return len(self.dev)
+
+    def __call__(self, loop: DecodeLoop, i: int, gamma: int) -> None:
+        d, t, tok, u = self.dev[i % len(self.dev)]
+        vd, vt, vtok, vu = loop.views(gamma)
+        with torch.cuda.stream(loop.stream):
+            vd.copy_(d[:, :gamma], non_blocking=True)
+            vt.copy_(t[:, :gamma + 1], non_blocking=True)
+            vtok.copy_(tok[:, :gamma], non_blocking=True)
+            vu.copy_(u[:, :gamma + 1], non_blocking=True)
+
+    def host_inputs(self, i: int, gamma: int):
+        """The host (storage-form) inputs iteration i verified at this gamma."""
+        from dataclasses import replace
+        x = self.inputs[i % len(self.inputs)]
+        return replace(x, draft=np.ascontiguousarray(x.draft[:, :gamma]),
+                       target=np.ascontiguousarray(x.target[:, :gamma + 1]),
+                       tokens=np.ascontiguousarray(x.tokens[:, :gamma]),
+                       uniforms=np.ascontiguousarray(x.uniforms[:, :gamma + 1]))
