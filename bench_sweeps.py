@@ -162,6 +162,40 @@ def sweep_alpha_beta(steps: int, warmup: int) -> dict:
     return {"sweep": "alpha_beta", "workload": base.name, "points": points}
 
 
+def sweep_top_k(steps: int, warmup: int) -> dict:
+    """Exact and sigmoid acceptance when both models' logits pass a top-k
+    processor (the rest -inf), on the fp16 sigmoid workload's shape, T = 0.7,
+    alpha = -beta = 1e4; time per step of both modes."""
+    import numpy as np
+    import torch
+
+    from paper_2406_11016_amd import binding
+    from paper_2406_11016_amd import workloads as W
+    base = W.WORKLOADS["sigmoid_b32_g10_v50272_f16_t0.7"]
+    points = []
+    for k in (1, 2, 5, 10, 20, 50, 200, 1000, 0):
+        w = base.with_(top_k=k)
+        x = W.generate(w, seed=base.seed * 10 + 1)
+        d, t, tok, uni = binding.to_device(x, "cuda")
+        out = {}
+        for mode in ("exact", "sigmoid"):
+            acc, nxt = binding.verify(d, t, tok, uni, mode=mode, temperature=w.temperature, alpha=w.alpha,
+                                      beta=w.beta)
+            torch.cuda.synchronize()
+            out[mode] = (acc.cpu().numpy(), nxt.cpu().numpy())
+        us = {m: _time_steps(w.with_(mode=m), x, steps, warmup) for m in ("exact", "sigmoid")}
+        le, ls = out["exact"][0], out["sigmoid"][0]
+        g = w.gamma
+        p = {"top_k": k if k else w.vocab, "accept_rate_exact": round(float(le[le >= 0].mean() / g), 4),
+             "accept_rate_sigmoid": round(float(ls[ls >= 0].mean() / g), 4),
+             "token_disagreement": round(float(((le != ls) | (out["exact"][1] != out["sigmoid"][1])).mean()), 4),
+             "us_per_step_exact": round(us["exact"], 3), "us_per_step_sigmoid": round(us["sigmoid"], 3),
+             "sentinels": int((le < 0).sum() + (ls < 0).sum()), "elements": int(le.size)}
+        log(json.dumps(p))
+        points.append(p)
+    return {"sweep": "top_k", "workload": base.name, "alpha": base.alpha, "beta": base.beta, "points": points}
+
+
 def decode_loop(iterations: int, gamma_max: int = 20, pool: int = 32) -> dict:
     """The decoding loop (gamma rule, one captured graph per gamma) on the B = 1
     workloads, against the same loop with eager calls."""
@@ -211,6 +245,8 @@ def run(kind: str, steps: int, warmup: int) -> int:
         out = sweep_gamma(steps, warmup)
     elif kind == "alpha_beta":
         out = sweep_alpha_beta(steps, warmup)
+    elif kind == "top_k":
+        out = sweep_top_k(steps, warmup)
     else:
         out = decode_loop(steps)
     out["seconds"] = round(time.perf_counter() - t0, 1)

@@ -172,6 +172,34 @@ sv_status_t spec_verify_sigmoid_probe(const void* draft_logits, const void* targ
                                       void* workspace, size_t workspace_bytes, hipStream_t stream,
                                       double* tau_out, float* weight_out, double* mass_out);
 
+/*
+ * Ragged variants: batch element b drafted gammas[b] tokens (1 <= gammas[b]
+ * <= gamma_max; `gammas` is a device array of B int32).  The tensors keep the
+ * padded shapes of gamma_max -- draft [B, gamma_max, V], target
+ * [B, gamma_max + 1, V], draft_tokens [B, gamma_max], uniforms
+ * [B, gamma_max + 1] -- and element b uses its draft rows 0..gammas[b]-1,
+ * target rows 0..gammas[b], tokens and acceptance uniforms 0..gammas[b]-1,
+ * and uniforms[b, gammas[b]] for the final draw; everything beyond is never
+ * read.  Each element is exactly the step of spec_verify_exact /
+ * spec_verify_sigmoid at its own gamma (Sec. 3.1 treats each sequence's drafts
+ * independently); accepted_len[b] lies in [0, gammas[b]].  An element whose
+ * gammas[b] lies outside 1 .. gamma_max gets the sentinel -1 in both outputs.
+ * The workspace is that of spec_verify_workspace_bytes(batch, gamma_max, ...).
+ * `gammas` NULL returns SV_ERR_NULL.
+ */
+sv_status_t spec_verify_exact_ragged(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                     const int32_t* draft_tokens, const float* uniforms, const int32_t* gammas,
+                                     int32_t batch, int32_t gamma_max, int32_t vocab, float temperature,
+                                     int32_t* accepted_len, int32_t* next_token,
+                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+sv_status_t spec_verify_sigmoid_ragged(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                       const int32_t* draft_tokens, const float* uniforms, const int32_t* gammas,
+                                       int32_t batch, int32_t gamma_max, int32_t vocab, float temperature,
+                                       float alpha, float beta,
+                                       int32_t* accepted_len, int32_t* next_token,
+                                       void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* spec_verify_status_string(sv_status_t status);
 

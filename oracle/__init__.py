@@ -15,4 +15,5 @@ from .spec_oracle import (  # noqa: F401
     sigmoid_approximation,
     softmax,
     verify,
+    verify_ragged,
 )

@@ -243,3 +243,39 @@ def verify(draft_logits: np.ndarray, target_logits: np.ndarray,
     return OracleResult(accepted_len, next_token, tau, final, mass,
                         np.where(bad, np.inf, acc_margin),
                         np.where(bad, np.inf, cdf_margin), fallback & ~bad)
+
+
+def verify_ragged(draft_logits: np.ndarray, target_logits: np.ndarray,
+                  draft_tokens: np.ndarray, uniforms: np.ndarray, gammas: np.ndarray, *, dtype: str,
+                  mode: str = "exact", temperature: float = 1.0,
+                  alpha: float = -1.0e4, beta: float = 1.0e4) -> OracleResult:
+    """Batch elements with their own number of drafts, in padded tensors.
+
+    Sec. 3.1 verifies each sequence's drafts on their own, so element ``b``
+    with ``g = gammas[b]`` drafts is exactly the step of :func:`verify` on its
+    draft rows ``0..g-1``, target rows ``0..g``, tokens ``0..g-1`` and
+    uniforms ``0..g`` (the last one driving the final draw); whatever the
+    padded tensors hold beyond that is not read.  An element with ``g``
+    outside ``1 .. gamma_max`` gets the sentinel.  ``tau`` is padded with NaN.
+    """
+    B, gmax, V = np.shape(draft_logits)
+    acc = np.full(B, SENTINEL, dtype=np.int64)
+    nxt = np.full(B, SENTINEL, dtype=np.int64)
+    tau = np.full((B, gmax), np.nan)
+    final = np.zeros((B, V))
+    mass = np.full(B, np.nan)
+    am = np.full(B, np.inf)
+    cm = np.full(B, np.inf)
+    fb = np.zeros(B, dtype=bool)
+    for b in range(B):
+        g = int(gammas[b])
+        if not 1 <= g <= gmax:
+            continue
+        o = verify(draft_logits[b:b + 1, :g], target_logits[b:b + 1, :g + 1], draft_tokens[b:b + 1, :g],
+                   uniforms[b:b + 1, :g + 1], dtype=dtype, mode=mode, temperature=temperature,
+                   alpha=alpha, beta=beta)
+        acc[b], nxt[b] = o.accepted_len[0], o.next_token[0]
+        tau[b, :g] = o.tau[0]
+        final[b], mass[b] = o.final_weights[0], o.mass[0]
+        am[b], cm[b], fb[b] = o.accept_margin[0], o.cdf_margin[0], o.fallback[0]
+    return OracleResult(acc, nxt, tau, final, mass, am, cm, fb)

@@ -29,6 +29,8 @@ SYMBOLS = (
     "spec_verify_sigmoid",
     "spec_verify_exact_probe",
     "spec_verify_sigmoid_probe",
+    "spec_verify_exact_ragged",
+    "spec_verify_sigmoid_ragged",
     "spec_verify_status_string",
 )
 
@@ -69,6 +71,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.spec_verify_exact_probe.restype = ctypes.c_int
     lib.spec_verify_sigmoid_probe.argtypes = common + [_f32, _f32] + outs + [_vp, _vp, _vp]
     lib.spec_verify_sigmoid_probe.restype = ctypes.c_int
+    ragged = [_vp, _vp, ctypes.c_int, _vp, _vp, _vp, _i32, _i32, _i32, _f32]
+    lib.spec_verify_exact_ragged.argtypes = ragged + outs
+    lib.spec_verify_exact_ragged.restype = ctypes.c_int
+    lib.spec_verify_sigmoid_ragged.argtypes = ragged + [_f32, _f32] + outs
+    lib.spec_verify_sigmoid_ragged.restype = ctypes.c_int
     lib.spec_verify_status_string.argtypes = [ctypes.c_int]
     lib.spec_verify_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -144,17 +151,25 @@ def _validate(draft, target, tokens, uniforms):
 def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, uniforms: torch.Tensor, *,
            mode: str = "exact", temperature: float = 1.0, alpha: float = -1.0e4, beta: float = 1.0e4,
            accepted_len: Optional[torch.Tensor] = None, next_token: Optional[torch.Tensor] = None,
-           workspace: Optional[torch.Tensor] = None, probe: bool = False):
+           workspace: Optional[torch.Tensor] = None, probe: bool = False, gammas: Optional[torch.Tensor] = None):
     """One verification step on the current stream.
 
     Returns ``(accepted_len, next_token)`` (int32 [B] device tensors), plus a
     :class:`Probe` when ``probe`` is true.  ``workspace`` (zero-filled before
-    its first use) may be passed to avoid an allocation per call.
+    its first use) may be passed to avoid an allocation per call.  ``gammas``
+    (int32 [B] device tensor) selects the ragged variant: element b uses its
+    first ``gammas[b]`` drafts of the padded tensors (no probes).
     """
     if mode not in ("exact", "sigmoid"):
         raise ValueError(mode)
     lib = load_library()
     B, g, V = _validate(draft, target, tokens, uniforms)
+    if gammas is not None:
+        if probe:
+            raise SpecVerifyError("the ragged variant has no probes")
+        if not gammas.is_cuda or gammas.dtype != torch.int32 or tuple(gammas.shape) != (B,) or \
+                not gammas.is_contiguous():
+            raise SpecVerifyError("gammas must be a contiguous int32 [B] device tensor")
     dev = draft.device
     if accepted_len is None:
         accepted_len = torch.empty(B, dtype=torch.int32, device=dev)
@@ -165,6 +180,15 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
     code = DTYPE_CODES[draft.dtype]
     head = [_ptr(draft), _ptr(target), code, _ptr(tokens), _ptr(uniforms), B, g, V, float(temperature)]
     tail = [_ptr(accepted_len), _ptr(next_token), _ptr(workspace), workspace.numel(), _stream(dev)]
+    if gammas is not None:
+        rhead = [_ptr(draft), _ptr(target), code, _ptr(tokens), _ptr(uniforms), _ptr(gammas), B, g, V,
+                 float(temperature)]
+        if mode == "exact":
+            st = lib.spec_verify_exact_ragged(*rhead, *tail)
+        else:
+            st = lib.spec_verify_sigmoid_ragged(*rhead, float(alpha), float(beta), *tail)
+        _check(st, f"spec_verify_{mode}_ragged")
+        return accepted_len, next_token
     pr = None
     if probe:
         pr = Probe(tau=torch.full((B, g), float("nan"), dtype=torch.float64, device=dev),

@@ -504,6 +504,7 @@ struct StepParams {
     int pstride;                   // stats words per batch element
     const int32_t* tokens;
     const float* uniforms;
+    const int32_t* gammas;         // ragged variant: drafts of each batch element (1 .. gamma)
     double temperature, alpha, beta;
     unsigned int* error;           // set to 1 if a wait ever timed out
     unsigned long long* dslot;     // [B, ncopy, kDecisionWords] copies of the published decision
@@ -538,6 +539,18 @@ struct Smem {
 // rows 0 .. gamma - 1, then draft rows 0 .. gamma - 1), target row gamma last.
 __device__ __forceinline__ int slot_row(int s, int gamma) { return s < gamma ? s : (s < 2 * gamma ? s + 1 : gamma); }
 
+// The number of drafts of batch element b: gamma, or in the ragged variant
+// gammas[b] when it lies in 1 .. gamma (otherwise gamma, and *bad is set: the
+// element's outputs are sentinels).
+template <bool kRagged>
+__device__ __forceinline__ int elem_gamma(const StepParams& P, int b, bool* bad) {
+    *bad = false;
+    if constexpr (!kRagged) return P.gamma;
+    const int g = P.gammas[b];
+    *bad = !(g >= 1 && g <= P.gamma);
+    return *bad ? P.gamma : g;
+}
+
 __device__ __forceinline__ double min1(double r) { return (r >= 1.0) ? 1.0 : r; }  // keeps NaN
 
 __device__ __forceinline__ void split3(double v, float& hi, float& mid, float& lo) {
@@ -552,14 +565,31 @@ __device__ __forceinline__ void split3(double v, float& hi, float& mid, float& l
 // S 2^K, merged later by exact power-of-two scaling.  Wave w streams the
 // contiguous quarter sub_chunk(k, w, ...) of the chunk; the quarters merge
 // in wave order.
-template <class D>
+template <class D, bool kRagged>
 __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot, int k, Smem& sm) {
     using T = typename D::T;
     constexpr int E = D::E;
     const int gamma = P.gamma, V = P.V;
     const float c = P.c;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int r = slot_row(slot, gamma);
+    int r = slot_row(slot, gamma);
+    if constexpr (kRagged) {
+        // element b drafts gb tokens: its rows are target 0 .. gb - 1, draft
+        // 0 .. gb - 1 and target gb (in the slot of target row gamma); the
+        // other slots publish an empty pair without reading anything
+        bool gbad;
+        const int gb = elem_gamma<true>(P, b, &gbad);
+        if (slot == 2 * gamma) {
+            r = gb;
+        } else if ((slot < gamma) ? (slot >= gb) : (slot - gamma >= gb)) {
+            if (threadIdx.x == 0) {
+                unsigned long long* out = P.pslot + (size_t)b * P.pstride + ((size_t)slot * P.nchunk1 + k) * 2;
+                publish(out, -INFINITY);
+                publish(out + 1, 0.0);
+            }
+            return;
+        }
+    }
     const int chunk = (slot == 2 * gamma && P.bonus_direct) ? P.chunkg : P.chunk1;
     const T* row = (r <= gamma) ? static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + r) * (size_t)V
                                 : static_cast<const T*>(P.draft) + ((size_t)b * gamma + (r - gamma - 1)) * (size_t)V;
@@ -698,7 +728,8 @@ __device__ __forceinline__ float row_kmax(Smem& sm, const float* K, int W) {
 }
 
 struct Decision {
-    int L;        // accepted length, in [0, gamma]
+    int L;        // accepted length, in [0, gb]
+    int gb;       // the element's number of drafts
     bool bad;     // sentinel
     bool ok;      // false if a wait timed out
     ExactWeights ew;
@@ -707,11 +738,13 @@ struct Decision {
 
 // The decision for batch element b: eq. (1) at the drafted tokens and the
 // first-rejection scan, plus the weights of the final distribution.
-template <class D, bool kExact>
+template <class D, bool kExact, bool kRagged>
 __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
     const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x;
+    bool gbad;
+    const int gb = elem_gamma<kRagged>(P, b, &gbad);
     const T* draft = static_cast<const T*>(P.draft) + (size_t)b * gamma * V;
     const T* target = static_cast<const T*>(P.target) + (size_t)b * (gamma + 1) * V;
 
@@ -720,7 +753,7 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     double r = 0.0;
     bool tok_ok = true;
     float zp = 0.0f, zq = 0.0f;
-    if (tid < gamma) {
+    if (tid < gb) {
         x = P.tokens[(size_t)b * gamma + tid];
         r = (double)P.uniforms[(size_t)b * (gamma + 1) + tid];
         tok_ok = (x >= 0 && x < V);
@@ -740,7 +773,7 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     }
 
     int stop = 0;
-    if (tid < gamma) {
+    if (tid < gb) {
         double tau;
         bool row_ok;
         if (kExact) {
@@ -769,15 +802,16 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     int first;
     bool first_bad, tok_bad;
     scan_stops(stop, tok_ok, sm, &first, &first_bad, &tok_bad);
-    d.L = min(first, gamma);
-    // with the bonus role, target row gamma is its business (it sentinels a
+    d.L = min(first, gb);
+    d.gb = gb;
+    // with the bonus role, target row gb is its business (it sentinels a
     // non-finite row itself)
-    d.bad = tok_bad || first_bad || !d.ok ||
-            (kExact && !P.bonus_direct && d.L == gamma && !isfinite(sm.rowL[2 * gamma]));
-    const bool two_rows = d.L < gamma;
+    d.bad = gbad || tok_bad || first_bad || !d.ok ||
+            (kExact && !P.bonus_direct && d.L == gb && !isfinite(sm.rowL[2 * gamma]));
+    const bool two_rows = d.L < gb;
     if (kExact && !d.bad && (two_rows || !P.bonus_direct)) {
         const double lp = sm.rowL[two_rows ? d.L : 2 * gamma];
-        const double lq = sm.rowL[gamma + min(d.L, gamma - 1)];
+        const double lq = sm.rowL[gamma + min(d.L, gb - 1)];
         d.ew.kind = two_rows ? kResidual : kTargetRow;
         d.ew.c = P.c;
         split3(lp, d.ew.kp, d.ew.lp_hi, d.ew.lp_lo);
@@ -890,15 +924,16 @@ __device__ __forceinline__ void wave_locate(double m, double u, Smem& sm) {
 // workgroup), which that reader clears once it has read it.  The decider also
 // writes the tau / normaliser probes and clears the stats words it read (it
 // is their only reader).
-template <class D, bool kExact>
+template <class D, bool kExact, bool kRagged>
 __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& sm) {
     const int gamma = P.gamma, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
-    const Decision d = decide<D, kExact>(P, b, sm);
+    const Decision d = decide<D, kExact, kRagged>(P, b, sm);
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     {
         const unsigned long long rec[kDecisionWords] = {
-            (unsigned long long)(d.L & 0xffff) | ((unsigned long long)(d.bad ? 1 : 0) << 16) | (1ull << 32),
+            (unsigned long long)(d.L & 0xffff) | ((unsigned long long)(d.bad ? 1 : 0) << 16) | (1ull << 32) |
+                ((unsigned long long)(d.gb & 0xffff) << 40),
             pack2(d.ew.kp, d.ew.lp_hi), pack2(d.ew.lp_lo, d.ew.kq), pack2(d.ew.lq_hi, d.ew.lq_lo),
             pack2(d.ew.d_hi, d.ew.d_lo)};
         unsigned long long* dst = P.dslot + (size_t)b * P.ncopy * kDecisionWords;
@@ -929,8 +964,9 @@ __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, in
     if ((int)threadIdx.x < kDecisionWords) clear_word(src + threadIdx.x);
     const unsigned long long w0 = sm.rec[0];
     d.L = d.ok ? (int)(w0 & 0xffff) : 0;
+    d.gb = d.ok ? (int)((w0 >> 40) & 0xffff) : P.gamma;
     d.bad = ((w0 >> 16) & 1) != 0 || !d.ok;
-    const int kind = (d.L < P.gamma) ? kResidual : kTargetRow;
+    const int kind = (d.L < d.gb) ? kResidual : kTargetRow;
     if (exact) {
         d.ew.kind = kind;
         d.ew.c = P.c;
@@ -956,13 +992,15 @@ __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, in
 // masses of the inverse-CDF draw are the sums S 2^(K - Kmax) of the row's
 // tile quarters, so the draw scans only the one quarter the uniform falls in
 // (one vector per thread).  It is the only reader of row gamma's words and clears them.
-template <class D>
+template <class D, bool kRagged>
 __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
     const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
     const int W = kWaves * P.nchunkg;  // quarters of the row's tiles
-    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
+    bool gbad;
+    const int gb = elem_gamma<kRagged>(P, b, &gbad);  // the row drawn from: target row gb
+    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gb];
     unsigned long long* rec = P.dslot + ((size_t)b * P.ncopy + P.ncopy - 1) * kDecisionWords;
     unsigned long long* words = P.pslot + (size_t)b * P.pstride + (size_t)2 * gamma * P.nchunk1 * 2;
     // one poll over the decision record and the row's (K, S) pairs
@@ -988,7 +1026,7 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     }
     const unsigned long long w0 = sm.rec[0];
     // otherwise b's draw workgroup writes b's outputs
-    const bool draw = ((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gamma;
+    const bool draw = ((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gb;
     if (!draw && P.lognorm_out == nullptr) return;
 
     // the masses S 2^(K - Kmax) of the row's chunks, their total and the chunk
@@ -1020,7 +1058,7 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
         j = mass_locate(sm.sub, W, u * total, loc, sm, &t_local);
     }
     const double lam = (double)km + log2(total);  // the row's log2-normaliser
-    if (P.lognorm_out != nullptr && tid == 0) P.lognorm_out[(size_t)b * R + gamma] = lam * 0.693147180559945309417;
+    if (P.lognorm_out != nullptr && tid == 0) P.lognorm_out[(size_t)b * R + gb] = lam * 0.693147180559945309417;
     if (!draw) return;
     // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
     int idx = -1;
@@ -1029,7 +1067,7 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
             const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunkg, V, D::E);
             const int begin = sp.begin;
             const int n = sp.n;
-            const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gamma) * V + begin;
+            const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V + begin;
             // scan on the quarter's own scale 2^K: its largest weight is at
             // least 1/2, so a quarter with positive mass has a positive weight
             ExactWeights w{};
@@ -1044,7 +1082,7 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     }
     const bool bad = idx < 0;
     if (tid == 0) {
-        P.accepted_len[b] = bad ? -1 : gamma;
+        P.accepted_len[b] = bad ? -1 : gb;
         P.next_token[b] = bad ? -1 : idx;
         // the draw's total in units of the row normaliser (1 up to rounding)
         if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total * exp2((double)km - lam);
@@ -1055,7 +1093,7 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
         w.kind = kTargetRow;
         w.c = P.c;
         split3(lam, w.kp, w.lp_hi, w.lp_lo);
-        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gamma) * V;
+        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V;
         for (int x = tid; x < V; x += kThreads)
             P.weight_out[(size_t)b * V + x] = w.template eval<kTargetRow>(to_f32(rp[x]), -INFINITY);
     }
@@ -1070,7 +1108,7 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
     const Decision d = read_decision(P, b, k2, kExact, sm);
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     // b's bonus workgroup draws when every draft is accepted: nothing to do here
-    const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == gamma;
+    const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == d.gb;
     if (drawn) return;
     const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
     double m = 0.0;
@@ -1096,13 +1134,13 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int M = P.nchunk2 * kWaves;
     Decision d = read_decision(P, b, P.nchunk2, kExact, sm);
-    const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == gamma;
+    const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == d.gb;
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (drawn) return;
     unsigned long long* ms = P.mslot + (size_t)b * M;
     const bool got = d.ok && wait_words(ms, M, sm.sub);
     if (d.ok && !got && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gamma];
+    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + d.gb];
     const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V;
     const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V;
     float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V : nullptr;
@@ -1130,7 +1168,7 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
             break;
         }
         if (total == 0.0) {
-            if (pass == 0 && L < gamma) {
+            if (pass == 0 && L < d.gb) {
                 // no residual mass (possible in sigmoid mode): draw from target row L
                 d.ew.kind = kTargetRow;
                 d.sw.kind = kTargetRow;
@@ -1169,7 +1207,7 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
     for (int i = tid; i < M; i += kThreads) clear_word(ms + i);
 }
 
-template <class D, bool kExact>
+template <class D, bool kExact, bool kRagged>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void verify_kernel(StepParams P) {
     __shared__ Smem sm;
     // one argument fetch for the role split and the stats role (see Layout)
@@ -1196,7 +1234,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         // target row gamma of every batch element, streamed last
         const int t = (int)(id - Y.end1);
         const int b = (int)Y.dcg.of((unsigned int)t);
-        stats_role<D>(P, b, 2 * P.gamma, t - b * P.nchunkg, sm);
+        stats_role<D, kRagged>(P, b, 2 * P.gamma, t - b * P.nchunkg, sm);
         return;
     } else if (id < Y.end2) {
         const unsigned int loc = id - Y.endg;
@@ -1204,17 +1242,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         r = loc - k * Y.size2 + (unsigned int)Y.S + 1u;
         bm = Y.b2 + (int)k;
     } else {
-        if (kExact) bonus_role<D>(P, (int)(id - Y.end2), sm);
+        if (kExact) bonus_role<D, kRagged>(P, (int)(id - Y.end2), sm);
         return;
     }
     const unsigned int S = (unsigned int)Y.S;
     if (r < S) {
         const int slot = (int)Y.dc1.of(r);
-        stats_role<D>(P, bs, slot, (int)r - slot * P.nchunk1, sm);
+        stats_role<D, kRagged>(P, bs, slot, (int)r - slot * P.nchunk1, sm);
         return;
     }
     if (r == S) {
-        decider_role<D, kExact>(P, bs, sm);
+        decider_role<D, kExact, kRagged>(P, bs, sm);
         return;
     }
     r -= S + 1u;
@@ -1359,6 +1397,7 @@ struct Call {
     float* weight_out;
     double* mass_out;
     double* lognorm_out;
+    const int32_t* gammas;  // ragged variant, else nullptr
 };
 
 template <class D>
@@ -1369,6 +1408,7 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.target = a.target;
     P.tokens = a.tokens;
     P.uniforms = a.uniforms;
+    P.gammas = a.gammas;
     P.B = a.B;
     P.gamma = a.gamma;
     P.V = a.V;
@@ -1404,10 +1444,18 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.weight_out = a.weight_out;
     P.mass_out = a.mass_out;
     P.lognorm_out = a.lognorm_out;
-    if (exact)
-        hipLaunchKernelGGL((verify_kernel<D, true>), dim3((unsigned int)n_total), dim3(kThreads), 0, a.stream, P);
-    else
-        hipLaunchKernelGGL((verify_kernel<D, false>), dim3((unsigned int)n_total), dim3(kThreads), 0, a.stream, P);
+    const dim3 grid((unsigned int)n_total), block(kThreads);
+    if (a.gammas == nullptr) {
+        if (exact)
+            hipLaunchKernelGGL((verify_kernel<D, true, false>), grid, block, 0, a.stream, P);
+        else
+            hipLaunchKernelGGL((verify_kernel<D, false, false>), grid, block, 0, a.stream, P);
+    } else {
+        if (exact)
+            hipLaunchKernelGGL((verify_kernel<D, true, true>), grid, block, 0, a.stream, P);
+        else
+            hipLaunchKernelGGL((verify_kernel<D, false, true>), grid, block, 0, a.stream, P);
+    }
     return hipGetLastError() == hipSuccess ? SV_OK : SV_ERR_HIP;
 }
 
@@ -1463,7 +1511,7 @@ sv_status_t spec_verify_exact(const void* draft_logits, const void* target_logit
                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
     sv::Call a{draft_logits, target_logits, dtype, draft_tokens, uniforms, batch, gamma, vocab, temperature,
                0.0f, 0.0f, accepted_len, next_token, workspace, workspace_bytes, stream,
-               nullptr, nullptr, nullptr, nullptr};
+               nullptr, nullptr, nullptr, nullptr, nullptr};
     return sv::run(a, true);
 }
 
@@ -1473,7 +1521,7 @@ sv_status_t spec_verify_sigmoid(const void* draft_logits, const void* target_log
                                 int32_t* next_token, void* workspace, size_t workspace_bytes, hipStream_t stream) {
     sv::Call a{draft_logits, target_logits, dtype, draft_tokens, uniforms, batch, gamma, vocab, temperature,
                alpha, beta, accepted_len, next_token, workspace, workspace_bytes, stream,
-               nullptr, nullptr, nullptr, nullptr};
+               nullptr, nullptr, nullptr, nullptr, nullptr};
     return sv::run(a, false);
 }
 
@@ -1484,7 +1532,7 @@ sv_status_t spec_verify_exact_probe(const void* draft_logits, const void* target
                                     float* weight_out, double* mass_out, double* lognorm_out) {
     sv::Call a{draft_logits, target_logits, dtype, draft_tokens, uniforms, batch, gamma, vocab, temperature,
                0.0f, 0.0f, accepted_len, next_token, workspace, workspace_bytes, stream,
-               tau_out, weight_out, mass_out, lognorm_out};
+               tau_out, weight_out, mass_out, lognorm_out, nullptr};
     return sv::run(a, true);
 }
 
@@ -1496,7 +1544,31 @@ sv_status_t spec_verify_sigmoid_probe(const void* draft_logits, const void* targ
                                       float* weight_out, double* mass_out) {
     sv::Call a{draft_logits, target_logits, dtype, draft_tokens, uniforms, batch, gamma, vocab, temperature,
                alpha, beta, accepted_len, next_token, workspace, workspace_bytes, stream,
-               tau_out, weight_out, mass_out, nullptr};
+               tau_out, weight_out, mass_out, nullptr, nullptr};
+    return sv::run(a, false);
+}
+
+sv_status_t spec_verify_exact_ragged(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                     const int32_t* draft_tokens, const float* uniforms, const int32_t* gammas,
+                                     int32_t batch, int32_t gamma_max, int32_t vocab, float temperature,
+                                     int32_t* accepted_len, int32_t* next_token, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream) {
+    if (gammas == nullptr) return SV_ERR_NULL;
+    sv::Call a{draft_logits, target_logits, dtype, draft_tokens, uniforms, batch, gamma_max, vocab, temperature,
+               0.0f, 0.0f, accepted_len, next_token, workspace, workspace_bytes, stream,
+               nullptr, nullptr, nullptr, nullptr, gammas};
+    return sv::run(a, true);
+}
+
+sv_status_t spec_verify_sigmoid_ragged(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                       const int32_t* draft_tokens, const float* uniforms, const int32_t* gammas,
+                                       int32_t batch, int32_t gamma_max, int32_t vocab, float temperature,
+                                       float alpha, float beta, int32_t* accepted_len, int32_t* next_token,
+                                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (gammas == nullptr) return SV_ERR_NULL;
+    sv::Call a{draft_logits, target_logits, dtype, draft_tokens, uniforms, batch, gamma_max, vocab, temperature,
+               alpha, beta, accepted_len, next_token, workspace, workspace_bytes, stream,
+               nullptr, nullptr, nullptr, nullptr, gammas};
     return sv::run(a, false);
 }
 

@@ -62,6 +62,7 @@ class Workload:
     temperature: float = 1.0
     alpha: float = -1.0e4   # sigmoid scaling constants (eq. (5)); unused in exact mode
     beta: float = 1.0e4
+    top_k: int = 0          # > 0: every row keeps its k largest logits, the rest are -inf
 
     @property
     def logit_bytes(self) -> int:
@@ -186,6 +187,20 @@ def gumbel_max_tokens(g: np.random.Generator, draft_f64: np.ndarray,
     return np.argmax(draft_f64 / temperature + gum, axis=-1).astype(np.int32)
 
 
+def mask_top_k(stored: np.ndarray, dtype: str, k: int) -> np.ndarray:
+    """A top-k logit processor: each row (last axis) keeps its k largest
+    stored logits (ties broken towards the lower index) and every other logit
+    becomes -inf.  k <= 0 or k >= V leaves the rows unchanged."""
+    V = stored.shape[-1]
+    if k <= 0 or k >= V:
+        return stored
+    vals = stored_as_float64(stored, dtype)
+    drop = np.argsort(-vals, axis=-1, kind="stable")[..., k:]
+    out = stored.copy()
+    np.put_along_axis(out, drop, encode(np.array([-np.inf]), dtype)[0], axis=-1)
+    return out
+
+
 def generate(w: Workload, seed: Optional[int] = None,
              batch_indices: Optional[range] = None) -> Inputs:
     """Generate the inputs of ``w``.  ``batch_indices`` selects a subset of the
@@ -204,8 +219,8 @@ def generate(w: Workload, seed: Optional[int] = None,
         g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, b])))
         base = _draw_base(g, w.base, w.base_scale, (G + 1, V))
         noise = g.normal(0.0, w.noise_scale, size=(G + 1, V))
-        draft[i] = encode(base[:G], w.dtype)
-        target[i] = encode(base + noise, w.dtype)
+        draft[i] = mask_top_k(encode(base[:G], w.dtype), w.dtype, w.top_k)
+        target[i] = mask_top_k(encode(base + noise, w.dtype), w.dtype, w.top_k)
         del base, noise
         tokens[i] = gumbel_max_tokens(g, stored_as_float64(draft[i], w.dtype), w.temperature)
         uniforms[i] = make_uniforms(g, G + 1)
@@ -216,9 +231,9 @@ def generate(w: Workload, seed: Optional[int] = None,
 def small_case(batch: int, gamma: int, vocab: int, dtype: str, mode: str = "exact",
                seed: int = 7, base_scale: float = 2.0, noise_scale: float = 0.5,
                temperature: float = 1.0, alpha: float = -1.0e4, beta: float = 1.0e4,
-               base: str = "normal") -> Inputs:
+               base: str = "normal", top_k: int = 0) -> Inputs:
     """A small workload of arbitrary shape with the same value law (tests)."""
     w = Workload(f"{mode}_b{batch}_g{gamma}_v{vocab}_{dtype}", mode, batch, gamma, vocab,
                  dtype, base, base_scale, noise_scale, seed=seed,
-                 temperature=temperature, alpha=alpha, beta=beta)
+                 temperature=temperature, alpha=alpha, beta=beta, top_k=top_k)
     return generate(w)

@@ -90,10 +90,31 @@ def _sigmoid(lib, a, alpha=-1e4, beta=1e4):
                                    a["ws_bytes"], a["stream"])
 
 
+def _ragged(lib, a, gammas=0x8000, sigmoid=False, alpha=-1e4, beta=1e4):
+    head = [a["draft"], a["target"], a["dtype"], a["tokens"], a["uniforms"], gammas, a["B"], a["gamma"], a["V"],
+            a["T"]]
+    tail = [a["acc"], a["nxt"], a["ws"], a["ws_bytes"], a["stream"]]
+    if sigmoid:
+        return lib.spec_verify_sigmoid_ragged(*head, alpha, beta, *tail)
+    return lib.spec_verify_exact_ragged(*head, *tail)
+
+
 @pytest.mark.parametrize("field", ["draft", "target", "tokens", "uniforms", "acc", "nxt", "ws"])
 def test_null_pointers_rejected(lib, field):
     assert _exact(lib, _args(**{field: None})) == SV_ERR_NULL
     assert _sigmoid(lib, _args(**{field: None})) == SV_ERR_NULL
+    assert _ragged(lib, _args(**{field: None})) == SV_ERR_NULL
+    assert _ragged(lib, _args(**{field: None}), sigmoid=True) == SV_ERR_NULL
+
+
+def test_ragged_checks(lib):
+    assert _ragged(lib, _args(), gammas=None) == SV_ERR_NULL
+    assert _ragged(lib, _args(), gammas=None, sigmoid=True) == SV_ERR_NULL
+    assert _ragged(lib, _args(gamma=129)) == SV_ERR_SHAPE
+    assert _ragged(lib, _args(T=0.0)) == SV_ERR_PARAM
+    assert _ragged(lib, _args(), sigmoid=True, alpha=1.0, beta=1.0) == SV_ERR_PARAM
+    need = lib.spec_verify_workspace_bytes(2, 3, 100, 0)
+    assert _ragged(lib, _args(ws_bytes=need - 1)) == SV_ERR_WORKSPACE
 
 
 def test_invalid_shapes_dtype_params_workspace(lib):

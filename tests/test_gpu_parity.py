@@ -131,6 +131,18 @@ def test_masked_logits(mode):
     compare(x, run_gpu(x), run_oracle(x), label=f"masked {mode}")
 
 
+@pytest.mark.parametrize("mode", ["exact", "sigmoid"])
+@pytest.mark.parametrize("k", [1, 3, 50, 2000])
+def test_top_k_masked_logits(mode, k):
+    # a top-k logit processor on both models: most logits -inf, different
+    # supports for draft and target (tokens outside the target's top-k are
+    # rejected, tokens inside are accepted with tau ~ 1 in sigmoid mode)
+    for dtype, V in (("f32", 5003), ("bf16", 20011)):
+        x = W.small_case(8, 6, V, dtype, mode=mode, seed=400 + k, top_k=k, alpha=-1e4, beta=1e4)
+        nflag = compare(x, run_gpu(x), run_oracle(x), label=f"top-{k} {dtype} {mode}")
+        _report(f"top-{k}", x, nflag)
+
+
 def test_fp16_extremes():
     x = W.small_case(4, 3, 1000, "f16", seed=31)
     x.target[0, 0, 10] = np.float16(65504.0)

@@ -69,3 +69,21 @@ def test_headline_workload_generates():
     assert x.draft.dtype == np.uint16 and x.draft.shape == (2, 8, 128256)
     vals = W.decode_bf16(x.target).astype(np.float64)
     assert np.isfinite(vals).all() and vals.max() > 20   # heavy tails
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+def test_top_k_mask_keeps_the_k_largest(dtype):
+    x = W.small_case(3, 4, 500, dtype, seed=5, top_k=7)
+    full = W.small_case(3, 4, 500, dtype, seed=5)
+    for masked, raw in ((x.draft, full.draft), (x.target, full.target)):
+        m = W.stored_as_float64(masked, dtype)
+        r = W.stored_as_float64(raw, dtype)
+        keep = np.isfinite(m)
+        assert np.all(keep.sum(axis=-1) == 7)
+        assert np.all(m[keep] == r[keep])                              # kept values unchanged
+        assert np.all(np.isneginf(m[~keep]))
+        kth = np.sort(r, axis=-1)[..., -7]
+        assert np.all(np.where(keep, r, np.inf).min(axis=-1) >= kth)   # the kept ones are the largest
+    # drafted tokens are drawn from the masked draft rows
+    d = W.stored_as_float64(x.draft, dtype)
+    assert np.all(np.isfinite(np.take_along_axis(d, x.tokens[..., None].astype(np.int64), axis=-1)))
