@@ -33,7 +33,7 @@ def log(msg: str) -> None:
     print(f"[sweep] {msg}", file=sys.stderr, flush=True)
 
 
-def _time_steps(w, x, steps: int, warmup: int, rotate_mb: float = 768.0) -> float:
+def _time_steps(w, x, steps: int, warmup: int, rotate_mb: float = 768.0, gammas=None) -> float:
     """Microseconds per call, HIP events on the launch stream, rotating input copies."""
     import torch
 
@@ -45,11 +45,12 @@ def _time_steps(w, x, steps: int, warmup: int, rotate_mb: float = 768.0) -> floa
     acc = torch.empty(w.batch, dtype=torch.int32, device=dev)
     nxt = torch.empty(w.batch, dtype=torch.int32, device=dev)
     ws = binding.new_workspace(w.batch, w.gamma, w.vocab, d0.dtype, dev)
+    gd = None if gammas is None else torch.as_tensor(gammas, dtype=torch.int32).to(dev)
 
     def step(i):
         d, t = sets[i % nrot]
         binding.verify(d, t, tok, uni, mode=w.mode, temperature=w.temperature, alpha=w.alpha, beta=w.beta,
-                       accepted_len=acc, next_token=nxt, workspace=ws)
+                       accepted_len=acc, next_token=nxt, workspace=ws, gammas=gd)
 
     for i in range(warmup):
         step(i)
@@ -196,6 +197,32 @@ def sweep_top_k(steps: int, warmup: int) -> dict:
     return {"sweep": "top_k", "workload": base.name, "alpha": base.alpha, "beta": base.beta, "points": points}
 
 
+def sweep_ragged(steps: int, warmup: int) -> dict:
+    """The ragged variant on the batched bf16 workload (B = 64, gamma_max = 8,
+    V = 128,256): time per step and the fraction of 8 TB/s on the bytes the
+    elements' own rows hold, sum_b (2 gammas[b] + 1) V s, for several
+    distributions of gammas[b]."""
+    import numpy as np
+
+    from paper_2406_11016_amd import workloads as W
+    w = W.WORKLOADS["exact_b64_g8_v128256_bf16"]
+    x = W.generate(w)
+    rng = np.random.default_rng(5)
+    dists = {"all 8 (plain shape)": np.full(w.batch, 8), "uniform 1..8": rng.integers(1, 9, size=w.batch),
+             "all 4": np.full(w.batch, 4), "all 1": np.full(w.batch, 1)}
+    us_plain = _time_steps(w, x, steps, warmup)
+    points = [{"gammas": "plain call (no gammas array)", "us_per_step": round(us_plain, 3),
+               "frac_of_8TBs": round(w.logit_bytes / (us_plain * 1e-6) / 8e12, 4)}]
+    for name, gam in dists.items():
+        us = _time_steps(w, x, steps, warmup, gammas=gam.astype(np.int32))
+        own = int(np.sum(2 * gam + 1)) * w.vocab * 2
+        p = {"gammas": name, "mean_gamma": round(float(gam.mean()), 3), "us_per_step": round(us, 3),
+             "own_row_bytes": own, "frac_of_8TBs": round(own / (us * 1e-6) / 8e12, 4)}
+        log(json.dumps(p))
+        points.append(p)
+    return {"sweep": "ragged", "workload": w.name, "points": points}
+
+
 def decode_loop(iterations: int, gamma_max: int = 20, pool: int = 32) -> dict:
     """The decoding loop (gamma rule, one captured graph per gamma) on the B = 1
     workloads, against the same loop with eager calls."""
@@ -247,6 +274,8 @@ def run(kind: str, steps: int, warmup: int) -> int:
         out = sweep_alpha_beta(steps, warmup)
     elif kind == "top_k":
         out = sweep_top_k(steps, warmup)
+    elif kind == "ragged":
+        out = sweep_ragged(steps, warmup)
     else:
         out = decode_loop(steps)
     out["seconds"] = round(time.perf_counter() - t0, 1)
