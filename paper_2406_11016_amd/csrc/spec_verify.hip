@@ -34,7 +34,8 @@ enum : int { kResidual = 0, kTargetRow = 1 };
 
 constexpr int kWantStatsTiles = 2048;    // enough workgroups to fill 256 CUs several times
 constexpr int kWantSampleTiles = 1024;
-constexpr int kStatsTileBytes = 65536;   // at most 64 KiB of one row per stats workgroup
+constexpr int kStatsTileBytes = 32768;   // at most 32 KiB of one row per stats workgroup
+constexpr long long kLagStreamBytes = 56000000;  // stream between an element's stats and its mass tiles
 constexpr int kGammaTileBytes = 16384;   // target rows gamma, streamed last: short tiles end the stream sharply
 constexpr int kSampleTileBytes = 32768;
 
@@ -1297,7 +1298,9 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     const long long min_elems = (long long)kThreads * E;
     const long long max_cells = std::max<long long>(1, ceil_div(V, min_elems));
 
-    // row chunks: enough workgroups to fill the GPU, at most 64 KiB each
+    // row chunks: enough workgroups to fill the GPU, at most 32 KiB each (smaller
+    // tiles end the stream sooner after their dispatch, but past ~10K
+    // workgroups per launch the dispatcher, not HBM, sets the pace)
     long long nc = ceil_div(kWantStatsTiles, B * R);
     nc = std::max(nc, ceil_div(V, kStatsTileBytes / s));
     nc = std::min(nc, max_cells);
@@ -1347,10 +1350,20 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
 
 // The layout for B batch elements: units with S stats tiles, a decider, Mt
 // mass tiles and a draw each; G stats tiles of the target rows gamma; Bd bonus
-// workgroups.  The mass and draw roles of b sit lagM = B / 4 units after its
-// stats: late enough that b's decision is usually published when they start
-// (a waiting workgroup holds a dispatch slot the stream needs), early enough
-// that most batch elements finish within the stream.
+// workgroups.  The mass and draw roles of b sit lagM units after its stats
+// (1 <= lagM <= B, see lag_units): late enough that b's decision is usually
+// published when they start (a waiting workgroup holds a dispatch slot the
+// stream needs), early enough that most batch elements finish within the
+// stream.
+// The lag in units: about kLagStreamBytes of stream (~9 us at 6.5 TB/s, the
+// time a decision takes to publish under load) behind the element's stats,
+// and all of them after the stream when the whole stream is shorter than
+// that (or absent: the sigmoid mode streams no rows).
+static long long lag_units(long long B, long long unit_bytes) {
+    if (unit_bytes <= 0) return B;
+    return std::min(B, std::max(1LL, ceil_div(kLagStreamBytes, unit_bytes)));
+}
+
 static Div make_div(unsigned int d) {
     unsigned int L = 0;
     while ((1ull << L) < d) ++L;
@@ -1358,8 +1371,8 @@ static Div make_div(unsigned int d) {
     return Div{(unsigned int)m, 31 + L};
 }
 
-static Layout make_layout(long long B, long long S, long long Mt, long long G, int nchunk1, int nchunkg) {
-    const long long lagM = std::max(1LL, B / 4);
+static Layout make_layout(long long B, long long S, long long Mt, long long G, int nchunk1, int nchunkg,
+                          long long lagM) {
     Layout y{};
     y.size0 = (unsigned int)(S + 1);
     y.size1 = (unsigned int)(S + Mt + 2);
@@ -1425,8 +1438,9 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.nslot = exact ? (direct ? 2 * a.gamma : 2 * a.gamma + 1) : 0;
     P.ncopy = pl.nchunk2 + (direct ? 2 : 1);
     P.pstride = (int)pl.pstride;
+    const long long unit_bytes = exact ? 2LL * a.gamma * (long long)a.V * (long long)sizeof(typename D::T) : 0;
     P.y = make_layout(a.B, (long long)P.nslot * pl.nchunk1, pl.nchunk2, direct ? (long long)a.B * pl.nchunkg : 0,
-                      pl.nchunk1, pl.nchunkg);
+                      pl.nchunk1, pl.nchunkg, lag_units(a.B, unit_bytes));
     const long long n_total = (long long)P.y.end2 + (direct ? a.B : 0);
     P.temperature = (double)a.temperature;
     P.alpha = (double)a.alpha;
