@@ -230,22 +230,37 @@ def decode_loop(iterations: int, gamma_max: int = 20, pool: int = 32) -> dict:
 
     from paper_2406_11016_amd import workloads as W
     from paper_2406_11016_amd.decode_loop import DecodeLoop, SyntheticSteps
+    import torch
     runs = []
     for name in ("exact_b1_g5_v51865_f32", "exact_b1_g10_v32000_f16"):
         w = W.WORKLOADS[name]
         src = SyntheticSteps(w, gamma_max=gamma_max, pool=pool)
-        for graphs in (True, False):
+        # the synthetic producer alone (four device copies per iteration from
+        # torch), at the loop's mean gamma, to separate it from the loop
+        probe = DecodeLoop(w.batch, w.vocab, w.dtype, mode=w.mode, gamma_max=gamma_max, use_graphs=False)
+        for i in range(20):
+            src(probe, i, 5)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(iterations):
+            src(probe, i, 5)
+        probe.stream.synchronize()
+        producer_us = (time.perf_counter() - t0) / iterations * 1e6
+        log(f"{name}: producer alone {producer_us:.1f} us per iteration")
+        for native, graphs in ((False, True), (False, False), (True, True), (True, False)):
             loop = DecodeLoop(w.batch, w.vocab, w.dtype, mode=w.mode, temperature=w.temperature, alpha=w.alpha,
-                              beta=w.beta, gamma0=5, gamma_max=gamma_max, use_graphs=graphs)
+                              beta=w.beta, gamma0=5, gamma_max=gamma_max, use_graphs=graphs, native=native)
             if graphs:
                 loop.capture_all()
-            loop.run(src, 20)                                   # warm-up
+            loop.run(src, 20)                                   # warm-up (captures the native graphs)
             t0 = time.perf_counter()
             st = loop.run(src, iterations)
             wall = time.perf_counter() - t0
-            dev = loop.run(src, min(iterations, 500), time_device=True).device_us
+            dev = loop.run(src, min(iterations, 500), time_device=True).device_us or [float("nan")]
+            loop.close()
             gam = np.array(st.gammas)
-            p = {"workload": name, "graphs": graphs, "iterations": iterations,
+            p = {"workload": name, "loop": "native" if native else "python", "graphs": graphs,
+                 "iterations": iterations, "producer_us_per_iteration": round(producer_us, 2),
                  "us_per_iteration": round(wall / iterations * 1e6, 2),
                  "tokens_per_iteration": round(st.tokens / iterations / w.batch, 3),
                  "tokens_per_s": round(st.tokens / wall, 1),
@@ -257,7 +272,9 @@ def decode_loop(iterations: int, gamma_max: int = 20, pool: int = 32) -> dict:
             runs.append(p)
     return {"sweep": "decode_loop", "gamma0": 5, "gamma_max": gamma_max, "runs": runs,
             "what": "iterations of: copy the next synthetic step's logits into the loop's static buffers, "
-                    "verify, copy L and the next token to pinned host memory, synchronise, apply the gamma rule"}
+                    "verify, copy L and the next token to pinned host memory, synchronise, apply the gamma rule; "
+                    "python = torch calls per iteration, native = one library call per iteration "
+                    "(spec_verify_loop_step); step_device_us only for the python loop"}
 
 
 def run(kind: str, steps: int, warmup: int) -> int:

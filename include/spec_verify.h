@@ -88,7 +88,9 @@ typedef enum sv_status {
     SV_ERR_DTYPE = -3,      /* unknown sv_dtype_t */
     SV_ERR_PARAM = -4,      /* temperature not finite and > 0; alpha/beta not finite with alpha < beta */
     SV_ERR_WORKSPACE = -5,  /* workspace smaller than spec_verify_workspace_bytes() or not 16-byte aligned */
-    SV_ERR_HIP = -6         /* a HIP launch failed (hipGetLastError after the launches) */
+    SV_ERR_HIP = -6,        /* a HIP launch failed (hipGetLastError after the launches), or a HIP
+                               call of the decoding loop failed */
+    SV_ERR_ALLOC = -7       /* the decoding loop could not allocate its host object */
 } sv_status_t;
 
 /* Largest number of drafted tokens per step supported by one call. */
@@ -199,6 +201,58 @@ sv_status_t spec_verify_sigmoid_ragged(const void* draft_logits, const void* tar
                                        float alpha, float beta,
                                        int32_t* accepted_len, int32_t* next_token,
                                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Decoding loop (Sec. 4, hyperparameters: the number of drafts starts at 5,
+ * grows by 2 after an iteration in which every draft was accepted and
+ * otherwise shrinks by 1; here it stays within 1 .. gamma_max, and with
+ * several batch elements every element must accept every draft to grow).
+ *
+ * The caller owns static buffers sized for gamma_max and, before each
+ * iteration, writes the iteration's inputs into their leading parts as the
+ * dense tensors of spec_verify_exact / spec_verify_sigmoid at that gamma
+ * (draft [B, gamma, V] at `draft`, target [B, gamma+1, V] at `target`,
+ * tokens [B, gamma], uniforms [B, gamma+1]), on `stream` or ordered before
+ * it.  spec_verify_loop_step then runs the step, copies accepted_len and
+ * next_token into `host_out` (pinned host memory, [2B] int32: the accepted
+ * lengths, then the next tokens), WAITS for the stream to finish (the host
+ * needs L to choose the next gamma and the tokens to append), and writes the
+ * next gamma.  With use_graphs the step and the two copies are captured into
+ * a HIP graph the first time each gamma is used and replayed afterwards.
+ *
+ * Ownership: every pointer in the descriptor is the caller's and must stay
+ * valid until spec_verify_loop_destroy; the loop allocates only its host
+ * object and the graphs.  The workspace must hold
+ * spec_verify_workspace_bytes(batch, g, vocab, dtype) for every g up to
+ * gamma_max (zero-filled before the first iteration; each iteration leaves it
+ * zero-filled).  One loop must not be stepped from two threads at once.
+ * Errors: SV_ERR_NULL, SV_ERR_SHAPE, SV_ERR_PARAM (mode not 0/1, gamma out
+ * of 1 .. gamma_max), SV_ERR_WORKSPACE at creation; the verification's own
+ * errors and SV_ERR_HIP at a step.
+ */
+typedef struct sv_loop sv_loop;
+
+typedef struct sv_loop_desc {
+    int32_t mode;                 /* 0: exact (spec_verify_exact), 1: sigmoid (spec_verify_sigmoid) */
+    sv_dtype_t dtype;
+    int32_t batch, gamma_max, vocab;
+    float temperature, alpha, beta;   /* alpha, beta: sigmoid mode only */
+    void* draft;                  /* device, B * gamma_max * V logits */
+    void* target;                 /* device, B * (gamma_max + 1) * V logits */
+    int32_t* tokens;              /* device, B * gamma_max */
+    float* uniforms;              /* device, B * (gamma_max + 1) */
+    int32_t* accepted_len;        /* device [B] */
+    int32_t* next_token;          /* device [B] */
+    int32_t* host_out;            /* pinned host [2B] */
+    void* workspace;
+    size_t workspace_bytes;
+    hipStream_t stream;
+    int32_t use_graphs;           /* nonzero: one captured graph per gamma */
+} sv_loop_desc_t;
+
+sv_status_t spec_verify_loop_create(const sv_loop_desc_t* desc, sv_loop** loop);
+sv_status_t spec_verify_loop_step(sv_loop* loop, int32_t gamma, int32_t* next_gamma);
+sv_status_t spec_verify_loop_destroy(sv_loop* loop);
 
 /* Static description of a status code. */
 const char* spec_verify_status_string(sv_status_t status);

@@ -31,6 +31,9 @@ SYMBOLS = (
     "spec_verify_sigmoid_probe",
     "spec_verify_exact_ragged",
     "spec_verify_sigmoid_ragged",
+    "spec_verify_loop_create",
+    "spec_verify_loop_step",
+    "spec_verify_loop_destroy",
     "spec_verify_status_string",
 )
 
@@ -40,6 +43,17 @@ class SpecVerifyError(RuntimeError):
 
 
 _lib = None
+
+
+class LoopDesc(ctypes.Structure):
+    """``sv_loop_desc_t`` of the decoding loop (see spec_verify.h)."""
+    _fields_ = [("mode", ctypes.c_int32), ("dtype", ctypes.c_int), ("batch", ctypes.c_int32),
+                ("gamma_max", ctypes.c_int32), ("vocab", ctypes.c_int32), ("temperature", ctypes.c_float),
+                ("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("draft", ctypes.c_void_p),
+                ("target", ctypes.c_void_p), ("tokens", ctypes.c_void_p), ("uniforms", ctypes.c_void_p),
+                ("accepted_len", ctypes.c_void_p), ("next_token", ctypes.c_void_p), ("host_out", ctypes.c_void_p),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t), ("stream", ctypes.c_void_p),
+                ("use_graphs", ctypes.c_int32)]
 
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
@@ -76,6 +90,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.spec_verify_exact_ragged.restype = ctypes.c_int
     lib.spec_verify_sigmoid_ragged.argtypes = ragged + [_f32, _f32] + outs
     lib.spec_verify_sigmoid_ragged.restype = ctypes.c_int
+    lib.spec_verify_loop_create.argtypes = [ctypes.POINTER(LoopDesc), ctypes.POINTER(ctypes.c_void_p)]
+    lib.spec_verify_loop_create.restype = ctypes.c_int
+    lib.spec_verify_loop_step.argtypes = [_vp, _i32, ctypes.POINTER(ctypes.c_int32)]
+    lib.spec_verify_loop_step.restype = ctypes.c_int
+    lib.spec_verify_loop_destroy.argtypes = [_vp]
+    lib.spec_verify_loop_destroy.restype = ctypes.c_int
     lib.spec_verify_status_string.argtypes = [ctypes.c_int]
     lib.spec_verify_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -226,3 +246,21 @@ def to_device(inputs, device="cuda"):
     return (d.to(device), t.to(device),
             torch.from_numpy(np.ascontiguousarray(inputs.tokens)).to(device),
             torch.from_numpy(np.ascontiguousarray(inputs.uniforms)).to(device))
+
+
+def loop_create(desc: LoopDesc) -> ctypes.c_void_p:
+    """A native decoding loop over the caller's buffers (spec_verify_loop_create)."""
+    h = ctypes.c_void_p()
+    _check(load_library().spec_verify_loop_create(ctypes.byref(desc), ctypes.byref(h)), "spec_verify_loop_create")
+    return h
+
+
+def loop_step(handle: ctypes.c_void_p, gamma: int) -> int:
+    """One iteration of the native loop (waits for it); returns the next gamma."""
+    nxt = ctypes.c_int32()
+    _check(load_library().spec_verify_loop_step(handle, int(gamma), ctypes.byref(nxt)), "spec_verify_loop_step")
+    return int(nxt.value)
+
+
+def loop_destroy(handle: ctypes.c_void_p) -> None:
+    _check(load_library().spec_verify_loop_destroy(handle), "spec_verify_loop_destroy")

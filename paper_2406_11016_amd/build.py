@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libspec_verify.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
-SOURCES = [os.path.join(CSRC, "spec_verify.hip")]
+SOURCES = [os.path.join(CSRC, "spec_verify.hip"), os.path.join(CSRC, "decode_loop.hip")]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

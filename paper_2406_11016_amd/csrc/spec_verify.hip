@@ -1595,6 +1595,7 @@ const char* spec_verify_status_string(sv_status_t status) {
         case SV_ERR_PARAM: return "invalid temperature or sigmoid scaling constants";
         case SV_ERR_WORKSPACE: return "workspace too small or misaligned";
         case SV_ERR_HIP: return "HIP launch failed";
+        case SV_ERR_ALLOC: return "host allocation failed";
     }
     return "unknown status";
 }

@@ -55,7 +55,7 @@ class DecodeLoop:
 
     def __init__(self, batch: int, vocab: int, dtype: str, *, mode: str = "exact", temperature: float = 1.0,
                  alpha: float = -1.0e4, beta: float = 1.0e4, gamma0: int = 5, gamma_max: int = 20,
-                 use_graphs: bool = True, device="cuda"):
+                 use_graphs: bool = True, native: bool = False, device="cuda"):
         if not (1 <= gamma0 <= gamma_max):
             raise ValueError("need 1 <= gamma0 <= gamma_max")
         self.B, self.V, self.dtype, self.mode = batch, vocab, dtype, mode
@@ -75,6 +75,29 @@ class DecodeLoop:
         self.ws = torch.zeros((ws + 15) // 16 * 16, dtype=torch.uint8, device=self.device)
         self.stream = torch.cuda.Stream(self.device)
         self.graphs: Dict[int, torch.cuda.CUDAGraph] = {}
+        # the native loop: one library call per iteration (graph replay or
+        # launch, the copies to pinned memory, the wait and the gamma rule)
+        self.native = None
+        if native:
+            desc = binding.LoopDesc(
+                mode=0 if mode == "exact" else 1, dtype=binding.DTYPE_CODES[tdt], batch=B, gamma_max=G, vocab=V,
+                temperature=temperature, alpha=alpha, beta=beta, draft=self.draft.data_ptr(),
+                target=self.target.data_ptr(), tokens=self.tokens.data_ptr(), uniforms=self.uniforms.data_ptr(),
+                accepted_len=self.acc.data_ptr(), next_token=self.nxt.data_ptr(), host_out=self.host.data_ptr(),
+                workspace=self.ws.data_ptr(), workspace_bytes=self.ws.numel(), stream=self.stream.cuda_stream,
+                use_graphs=1 if use_graphs else 0)
+            self.native = binding.loop_create(desc)
+
+    def close(self) -> None:
+        if self.native is not None:
+            binding.loop_destroy(self.native)
+            self.native = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
     # -- the buffers an iteration's producer writes ---------------------------
     def views(self, gamma: int) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
@@ -106,6 +129,8 @@ class DecodeLoop:
 
     def capture_all(self) -> None:
         """Capture every gamma up front (keeps capture out of a timed loop)."""
+        if self.native is not None:
+            return
         for g in range(1, self.gamma_max + 1):
             self._graph(g)
 
@@ -140,6 +165,17 @@ class DecodeLoop:
         ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) if time_device else None
         for i in range(iterations):
             producer(self, i, gamma)
+            if self.native is not None:
+                nxt_gamma = binding.loop_step(self.native, gamma)
+                h = self.host.numpy()
+                L, nx = h[:self.B].copy(), h[self.B:].copy()
+                stats.iterations += 1
+                stats.gammas.append(gamma)
+                stats.accepted.append(L)
+                stats.next_tokens.append(nx)
+                stats.tokens += int(np.sum(np.where(L >= 0, L + 1, 0)))
+                gamma = nxt_gamma
+                continue
             if ev is not None:
                 ev[0].record(self.stream)
             self.launch(gamma)

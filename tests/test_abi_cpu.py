@@ -156,3 +156,34 @@ def test_no_cpu_fallback_in_binding():
         if f.endswith(".py"):
             assert "import oracle" not in open(os.path.join(ROOT, "paper_2406_11016_amd", f)).read()
             assert "from oracle" not in open(os.path.join(ROOT, "paper_2406_11016_amd", f)).read()
+
+
+def _loop_desc(**kw):
+    d = dict(mode=0, dtype=0, batch=2, gamma_max=6, vocab=100, temperature=1.0, alpha=-1.0, beta=1.0,
+             draft=0x1000, target=0x2000, tokens=0x3000, uniforms=0x4000, accepted_len=0x5000, next_token=0x6000,
+             host_out=0x7000, workspace=0x8000, workspace_bytes=1 << 22, stream=None, use_graphs=1)
+    d.update(kw)
+    return binding.LoopDesc(**d)
+
+
+def test_loop_create_checks(lib):
+    """The native decoding loop validates its descriptor before touching the GPU."""
+    import ctypes
+    h = ctypes.c_void_p()
+    assert lib.spec_verify_loop_create(None, ctypes.byref(h)) == SV_ERR_NULL
+    for field in ("draft", "target", "tokens", "uniforms", "accepted_len", "next_token", "host_out", "workspace"):
+        assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(**{field: None})), ctypes.byref(h)) == SV_ERR_NULL
+    assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(mode=2)), ctypes.byref(h)) == SV_ERR_PARAM
+    assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(gamma_max=0)), ctypes.byref(h)) == SV_ERR_SHAPE
+    assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(gamma_max=129)), ctypes.byref(h)) == SV_ERR_SHAPE
+    need = max(lib.spec_verify_workspace_bytes(2, g, 100, 0) for g in range(1, 7))
+    assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(workspace_bytes=need - 1)),
+                                       ctypes.byref(h)) == SV_ERR_WORKSPACE
+    # a valid descriptor: the host object only (graphs come with the first step)
+    assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(workspace_bytes=need)), ctypes.byref(h)) == 0
+    nxt = ctypes.c_int32()
+    assert lib.spec_verify_loop_step(h, 0, ctypes.byref(nxt)) == SV_ERR_PARAM
+    assert lib.spec_verify_loop_step(h, 7, ctypes.byref(nxt)) == SV_ERR_PARAM
+    assert lib.spec_verify_loop_step(None, 3, ctypes.byref(nxt)) == SV_ERR_NULL
+    assert lib.spec_verify_loop_destroy(h) == 0
+    assert lib.spec_verify_loop_destroy(None) == 0

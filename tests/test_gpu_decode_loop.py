@@ -44,13 +44,21 @@ def test_decode_loop_matches_oracle_and_rule(case):
         loop = DecodeLoop(w.batch, w.vocab, w.dtype, mode=w.mode, temperature=w.temperature, alpha=w.alpha,
                           beta=w.beta, gamma0=5, gamma_max=gmax, use_graphs=graphs)
         runs[graphs] = loop.run(src, iters)
+    for graphs in (True, False):
+        loop = DecodeLoop(w.batch, w.vocab, w.dtype, mode=w.mode, temperature=w.temperature, alpha=w.alpha,
+                          beta=w.beta, gamma0=5, gamma_max=gmax, use_graphs=graphs, native=True)
+        runs[("native", graphs)] = loop.run(src, iters)
+        loop.close()
     st = runs[True]
-    # replayed graphs and eager calls: identical trajectories and outputs
-    assert st.gammas == runs[False].gammas
-    for a, b in zip(st.accepted, runs[False].accepted):
-        assert np.array_equal(a, b)
-    for a, b in zip(st.next_tokens, runs[False].next_tokens):
-        assert np.array_equal(a, b)
+    # replayed graphs, eager calls and the native loop (with and without its
+    # own graphs): identical trajectories and outputs
+    for key in (False, ("native", True), ("native", False)):
+        other = runs[key]
+        assert st.gammas == other.gammas, key
+        for a, b in zip(st.accepted, other.accepted):
+            assert np.array_equal(a, b), key
+        for a, b in zip(st.next_tokens, other.next_tokens):
+            assert np.array_equal(a, b), key
     # the rule, and the oracle on each iteration's inputs
     assert st.gammas[0] == 5
     grew = shrank = 0
