@@ -2,7 +2,7 @@
 //
 // Method: arXiv 2406.11016, Sec. 3.1 (eqs. (1)-(3)) and Sec. 3.2.2 (eqs. (4)-(5)).
 //
-// One launch per call.  Workgroups play one of four roles by index (see
+// One launch per call.  Workgroups play one of five roles by index (see
 // verify_kernel):
 //   stats    (exact mode) one chunk of one logit row, streamed once with
 //            128-bit non-temporal loads: the chunk's contribution to the row's
@@ -16,6 +16,8 @@
 //   draw     b: fixed-order prefix over b's sub-chunk masses, then one
 //            workgroup scan inside the sub-chunk the uniform falls in -- the
 //            inverse-CDF draw of the next token.
+//   bonus    b (exact mode): when every draft is accepted, the draw from
+//            target row gamma straight from that row's normaliser partials.
 // Sigmoid mode (eq. (5)) has no stats role: it needs no row normaliser, so
 // only the logits at the drafted tokens and the row(s) the next token is
 // drawn from are read.
