@@ -28,26 +28,34 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(w) -> int:
+def algorithmic_bytes(w, accepted_len=None) -> int:
     """Bytes a step must move at least: exact mode reads every logit once
     (B (2 gamma + 1) V s); sigmoid mode reads the drafted-token logits and the
-    row(s) the next token is drawn from (counted as the two-row residual case).
-    Plus tokens, uniforms and the two outputs."""
+    row(s) the next token is drawn from -- one row for an element that
+    accepts every draft, two otherwise (all elements counted as two when
+    ``accepted_len`` is not given).  Plus tokens, uniforms and the two
+    outputs."""
     from paper_2406_11016_amd.workloads import BYTES_PER_LOGIT
     s = BYTES_PER_LOGIT[w.dtype]
     small = w.batch * (w.gamma * 4 + (w.gamma + 1) * 4 + 2 * 4)
     if w.mode == "exact":
         return w.batch * (2 * w.gamma + 1) * w.vocab * s + small
-    return w.batch * (2 * w.gamma * s + 2 * w.vocab * s) + small
+    if accepted_len is None:
+        rows = 2 * w.batch
+    else:
+        rows = sum(1 if int(L) == w.gamma else 2 for L in accepted_len)
+    return w.batch * 2 * w.gamma * s + rows * w.vocab * s + small
+
+
+KERNEL_SOURCES = ("spec_verify.hip", "sv_device.hpp")
 
 
 def source_hash() -> str:
-    """sha256 prefix of the kernel sources (to match recorded counter data)."""
-    import glob
+    """sha256 prefix of the kernel's sources (to match recorded counter data)."""
     import hashlib
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2406_11016_amd", "csrc", "*"))):
-        with open(f, "rb") as fh:
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2406_11016_amd", "csrc", name), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
@@ -359,7 +367,7 @@ def main() -> int:
     if bool(((a < 0) | (a > w.gamma)).any()) or bool(((n < 0) | (n >= w.vocab)).any()):
         log("warning: sentinel outputs in the timed workload")
 
-    alg = algorithmic_bytes(w)
+    alg = algorithmic_bytes(w, a.numpy())
     achieved = alg / (ms_per_step * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": recorded_traffic(w.name),
