@@ -288,3 +288,39 @@ def test_gpu_emits_target_distribution_tiny_vocab():
         counts = np.bincount(emitted, minlength=V)
         sigma = np.sqrt(m * P[c] * (1 - P[c]))
         assert np.all(np.abs(counts - m * P[c]) <= 3 * sigma), (c, counts, m * P[c], sigma)
+
+
+# --- seeded random shapes ------------------------------------------------------
+
+def test_randomized_shapes():
+    """60 seeded random cases: batch 1-9, gamma 1-24, V 1-6000, every dtype and
+    mode, temperature 0.3-2, noise from near-identical to unrelated rows, some
+    with top-k masks, some ragged."""
+    rng = np.random.default_rng(20261202)
+    for case in range(60):
+        B = int(rng.integers(1, 10))
+        g = int(rng.integers(1, 25))
+        V = int(rng.choice([1, 2, 3, 17, 64, 255, 1000, 2049, 4096, 5999]))
+        dtype = str(rng.choice(["f32", "f16", "bf16"]))
+        mode = str(rng.choice(["exact", "sigmoid"]))
+        T = float(rng.choice([0.3, 0.7, 1.0, 2.0]))
+        noise = float(rng.choice([0.01, 0.2, 1.0, 4.0]))
+        top_k = int(rng.choice([0, 0, 0, 1, 5, 50]))
+        ab = float(rng.choice([10.0, 1e3, 1e4]))
+        x = W.small_case(B, g, V, dtype, mode=mode, seed=5000 + case, temperature=T, noise_scale=noise,
+                         top_k=top_k, alpha=-ab, beta=ab)
+        label = f"case {case}: B={B} g={g} V={V} {dtype} {mode} T={T} noise={noise} k={top_k}"
+        if case % 4 == 3:
+            gam = rng.integers(1, g + 1, size=B).astype(np.int32)
+            d, t, tok, u = binding.to_device(x, "cuda")
+            acc, nxt = binding.verify(d, t, tok, u, mode=mode, temperature=T, alpha=-ab, beta=ab,
+                                      gammas=torch.from_numpy(gam).to("cuda"))
+            torch.cuda.synchronize()
+            with np.errstate(all="ignore"):
+                o = oracle.verify_ragged(x.draft, x.target, x.tokens, x.uniforms, gam, dtype=dtype, mode=mode,
+                                         temperature=T, alpha=-ab, beta=ab)
+            ok = ~o.flagged(1e-6)
+            assert np.array_equal(acc.cpu().numpy()[ok], o.accepted_len[ok]), label
+            assert np.array_equal(nxt.cpu().numpy()[ok], o.next_token[ok]), label
+        else:
+            compare(x, run_gpu(x), run_oracle(x), label=label)
