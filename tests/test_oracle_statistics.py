@@ -113,3 +113,28 @@ def test_sigmoid_mode_first_token_law(alpha, beta, seed):
     k = int(np.sum(law > 0))
     nsigma = float(scipy.stats.norm.isf(1e-4 / (2 * k)))
     _check_counts(emitted[:, 0], law, "sigmoid position 0", nsigma=nsigma)
+
+
+def test_sigmoid_against_exact_on_the_sigmoid_workload():
+    """On unmasked logits at alpha = -beta = 1e4 the sigmoid approximation
+    accepts essentially every draft: with u = (z/T - alpha)/(beta - alpha)
+    = 0.5 + O(z/(2 T beta)), p_hat/q_hat = 1 + O((z_p - z_q)/(4 T beta)), so a
+    draft is rejected only when r_c lands within ~1e-4 of 1 (Sec. 3.2.2,
+    eq. (5)).  The exact mode on the same inputs accepts far fewer, and its
+    final-token distributions differ from the sigmoid ones almost entirely.
+    One input set of the named workload (32 elements, gamma = 10)."""
+    from paper_2406_11016_amd import workloads as W
+    w = W.WORKLOADS["sigmoid_b32_g10_v50272_f16_t0.7"]
+    x = W.generate(w, seed=w.seed * 100)
+    with np.errstate(all="ignore"):
+        e = verify(x.draft, x.target, x.tokens, x.uniforms, dtype=x.dtype, mode="exact", temperature=x.temperature)
+        s = verify(x.draft, x.target, x.tokens, x.uniforms, dtype=x.dtype, mode="sigmoid",
+                   temperature=x.temperature, alpha=x.alpha, beta=x.beta)
+    acc_e, acc_s = e.accepted_len.mean() / w.gamma, s.accepted_len.mean() / w.gamma
+    same = e.accepted_len == s.accepted_len
+    tv = 0.5 * np.abs(e.final_weights[same] - s.final_weights[same]).sum(axis=-1)
+    print(f"[oracle] exact acceptance {acc_e:.3f}, sigmoid {acc_s:.3f}, same row for {int(same.sum())} "
+          f"elements, mean TV {tv.mean() if tv.size else float('nan'):.3f}")
+    assert acc_s == 1.0
+    assert 0.1 < acc_e < 0.5
+    assert tv.size == 0 or tv.mean() > 0.5
