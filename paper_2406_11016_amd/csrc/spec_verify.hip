@@ -989,12 +989,13 @@ __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, in
     return d;
 }
 
-// b's bonus workgroup (exact mode): waits for its copy of b's decision and
-// for target row gamma's stats (which stream last), and, if every draft was
-// accepted, draws the next token from that row and writes b's outputs.  The
+// b's bonus workgroup (exact mode): waits for target row gamma's stats (which
+// stream last), draws the next token from that row, then reads its copy of
+// b's decision and, if every draft was accepted, writes b's outputs.  The
 // masses of the inverse-CDF draw are the sums S 2^(K - Kmax) of the row's
 // tile quarters, so the draw scans only the one quarter the uniform falls in
-// (one vector per thread).  It is the only reader of row gamma's words and clears them.
+// (one vector per thread).  It is the only reader of row gamma's words and
+// of its decision copy, and clears them.
 template <class D, bool kRagged>
 __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
@@ -1006,31 +1007,26 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gb];
     unsigned long long* rec = P.dslot + ((size_t)b * P.ncopy + P.ncopy - 1) * kDecisionWords;
     unsigned long long* words = P.pslot + (size_t)b * P.pstride + (size_t)2 * gamma * P.nchunk1 * 2;
-    // one poll over the decision record and the row's (K, S) pairs
-    const bool ok = poll_at<4>(
-        kDecisionWords + 2 * W,
-        [&](int i) { return (i < kDecisionWords) ? rec + i : words + (i - kDecisionWords); },
-        [&](int i, unsigned long long w) {
-            if (i < kDecisionWords) {
-                sm.rec[i] = ~w;
-            } else {
-                const int j = i - kDecisionWords;
-                if (j & 1)
-                    sm.S[j >> 1] = decode_word(w);
-                else
-                    sm.K[j >> 1] = (float)decode_word(w);
-            }
-        });
-    for (int i = tid; i < kDecisionWords + 2 * W; i += kThreads)
-        clear_word((i < kDecisionWords) ? rec + i : words + (i - kDecisionWords));
+    // the row's (K, S) pairs first: the draw does not depend on the decision,
+    // so it runs while b's decider may still be at work (the last elements'
+    // decisions publish after the stream has ended), and the decision is read
+    // only before the outputs are written
+    const bool ok = poll_at<4>(2 * W, [&](int i) { return words + i; }, [&](int i, unsigned long long w) {
+        if (i & 1)
+            sm.S[i >> 1] = decode_word(w);
+        else
+            sm.K[i >> 1] = (float)decode_word(w);
+    });
+    for (int i = tid; i < 2 * W; i += kThreads) clear_word(words + i);
     if (!ok) {
         if (tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (tid < kDecisionWords) clear_word(rec + tid);
         return;
     }
-    const unsigned long long w0 = sm.rec[0];
-    // otherwise b's draw workgroup writes b's outputs
-    const bool draw = ((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gb;
-    if (!draw && P.lognorm_out == nullptr) return;
+    // a first look at the decision, in flight during the draw (it is usually
+    // published by now; if not, it is polled for after the draw)
+    unsigned long long rw = 0ull;
+    if (tid < kDecisionWords) rw = __hip_atomic_load(rec + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
     // the masses S 2^(K - Kmax) of the row's chunks, their total and the chunk
     // the uniform falls in
@@ -1062,7 +1058,6 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     }
     const double lam = (double)km + log2(total);  // the row's log2-normaliser
     if (P.lognorm_out != nullptr && tid == 0) P.lognorm_out[(size_t)b * R + gb] = lam * 0.693147180559945309417;
-    if (!draw) return;
     // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
     int idx = -1;
     if (isfinite(total) && total > 0.0) {
@@ -1083,6 +1078,24 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
             idx = (local >= 0) ? begin + local : -1;
         }
     }
+    // b's decision (its copy for this workgroup, cleared once read): the
+    // outputs are this workgroup's only if every draft was accepted, otherwise
+    // b's draw workgroup writes them
+    bool rok = true;
+    if (__syncthreads_and(tid >= kDecisionWords || rw != 0ull)) {
+        if (tid < kDecisionWords) sm.rec[tid] = ~rw;
+        __syncthreads();
+    } else {
+        rok = wait_raw(rec, kDecisionWords, sm.rec);
+    }
+    if (tid < kDecisionWords) clear_word(rec + tid);
+    if (!rok) {
+        if (tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const unsigned long long w0 = sm.rec[0];
+    const bool draw = ((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gb;
+    if (!draw) return;
     const bool bad = idx < 0;
     if (tid == 0) {
         P.accepted_len[b] = bad ? -1 : gb;
