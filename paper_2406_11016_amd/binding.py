@@ -135,8 +135,10 @@ def new_workspace(batch: int, gamma: int, vocab: int, dtype, device) -> torch.Te
 
 
 def init_workspace(ws: torch.Tensor) -> None:
+    """Zero-fill a workspace on the current stream (e.g. after a timed-out wait)."""
     lib = load_library()
-    _check(lib.spec_verify_workspace_init(_ptr(ws), ws.numel() // 16 * 16, _stream(ws.device)),
+    nbytes = ws.numel() * ws.element_size()
+    _check(lib.spec_verify_workspace_init(_ptr(ws), nbytes // 16 * 16, _stream(ws.device)),
            "spec_verify_workspace_init")
 
 
@@ -154,6 +156,8 @@ def _validate(draft, target, tokens, uniforms):
             raise SpecVerifyError(f"{name} must be a device tensor")
         if not t.is_contiguous():
             raise SpecVerifyError(f"{name} must be contiguous")
+        if t.device != draft.device:
+            raise SpecVerifyError(f"{name} is on {t.device}, draft on {draft.device}")
     if draft.dtype not in DTYPE_CODES or target.dtype != draft.dtype:
         raise SpecVerifyError(f"logits must share one of {list(DTYPE_CODES)}; got {draft.dtype}/{target.dtype}")
     if draft.dim() != 3 or target.dim() != 3:
@@ -184,22 +188,29 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
         raise ValueError(mode)
     lib = load_library()
     B, g, V = _validate(draft, target, tokens, uniforms)
+    dev = draft.device
     if gammas is not None:
         if probe:
             raise SpecVerifyError("the ragged variant has no probes")
-        if not gammas.is_cuda or gammas.dtype != torch.int32 or tuple(gammas.shape) != (B,) or \
+        if gammas.device != dev or gammas.dtype != torch.int32 or tuple(gammas.shape) != (B,) or \
                 not gammas.is_contiguous():
-            raise SpecVerifyError("gammas must be a contiguous int32 [B] device tensor")
-    dev = draft.device
+            raise SpecVerifyError(f"gammas must be a contiguous int32 [{B}] tensor on {dev}")
     if accepted_len is None:
         accepted_len = torch.empty(B, dtype=torch.int32, device=dev)
     if next_token is None:
         next_token = torch.empty(B, dtype=torch.int32, device=dev)
+    for name, t in (("accepted_len", accepted_len), ("next_token", next_token)):
+        # the kernel writes B entries: anything else would be written out of bounds
+        if t.dtype != torch.int32 or tuple(t.shape) != (B,) or not t.is_contiguous() or t.device != dev:
+            raise SpecVerifyError(f"{name} must be a contiguous int32 [{B}] tensor on {dev}")
     if workspace is None:
         workspace = new_workspace(B, g, V, draft.dtype, dev)
+    elif not workspace.is_contiguous() or workspace.device != dev:
+        raise SpecVerifyError(f"workspace must be a contiguous tensor on {dev}")
     code = DTYPE_CODES[draft.dtype]
     head = [_ptr(draft), _ptr(target), code, _ptr(tokens), _ptr(uniforms), B, g, V, float(temperature)]
-    tail = [_ptr(accepted_len), _ptr(next_token), _ptr(workspace), workspace.numel(), _stream(dev)]
+    tail = [_ptr(accepted_len), _ptr(next_token), _ptr(workspace), workspace.numel() * workspace.element_size(),
+            _stream(dev)]
     if gammas is not None:
         rhead = [_ptr(draft), _ptr(target), code, _ptr(tokens), _ptr(uniforms), _ptr(gammas), B, g, V,
                  float(temperature)]
