@@ -324,3 +324,42 @@ def test_randomized_shapes():
             assert np.array_equal(nxt.cpu().numpy()[ok], o.next_token[ok]), label
         else:
             compare(x, run_gpu(x), run_oracle(x), label=label)
+
+
+def test_determinism_at_the_headline_shape():
+    """1000 back-to-back calls on the headline workload give bit-identical
+    outputs (every reduction has a fixed order; no float atomics)."""
+    x = W.generate(W.WORKLOADS["exact_b64_g8_v128256_bf16"])
+    d, t, tok, u = binding.to_device(x, "cuda")
+    ws = binding.new_workspace(x.batch, x.gamma, x.vocab, d.dtype, "cuda")
+    a0, n0 = binding.verify(d, t, tok, u, workspace=ws)
+    a0, n0 = a0.clone(), n0.clone()
+    acc = torch.empty_like(a0)
+    nxt = torch.empty_like(n0)
+    same = torch.ones((), dtype=torch.bool, device="cuda")
+    for _ in range(1000):
+        binding.verify(d, t, tok, u, accepted_len=acc, next_token=nxt, workspace=ws)
+        same &= (acc == a0).all() & (nxt == n0).all()
+    torch.cuda.synchronize()
+    assert bool(same)
+    assert int(torch.count_nonzero(ws)) == 0
+
+
+def test_decisions_do_not_depend_on_the_batch_tiling():
+    """The same batch elements verified inside the full batch (B = 64: 32 KiB
+    chunks, bonus tiles), as a batch of 8 and one by one (B = 1: one vector
+    per thread) take different chunkings and layouts; the decisions agree
+    everywhere the oracle does not flag a threshold."""
+    w = W.WORKLOADS["exact_b64_g8_v128256_bf16"]
+    x = W.generate(w)
+    sub = W.generate(w, batch_indices=range(8))
+    o = run_oracle(sub)
+    ok = ~o.flagged(1e-6)
+    full = run_gpu(x, probe=False)
+    eight = run_gpu(sub, probe=False)
+    singles = [run_gpu(W.generate(w, batch_indices=range(b, b + 1)), probe=False) for b in range(8)]
+    one_acc = np.array([s[0][0] for s in singles])
+    one_nxt = np.array([s[1][0] for s in singles])
+    for acc, nxt in ((full[0][:8], full[1][:8]), eight, (one_acc, one_nxt)):
+        assert np.array_equal(acc[ok], o.accepted_len[ok])
+        assert np.array_equal(nxt[ok], o.next_token[ok])
