@@ -904,8 +904,15 @@ __device__ __forceinline__ int mass_locate(const double* m, int M, double t, con
 // positive mass, if rounding leaves t at or beyond the total; -1 if no mass
 // is positive -- sm.cross_t the part of t inside it and sm.cross_tot the
 // total.  The caller's barrier publishes them.
-__device__ __forceinline__ void wave_locate(double m, double u, Smem& sm) {
-    const int lane = threadIdx.x % kWave;
+// (wave_locate_r returns the results in registers, valid in every lane of the
+// wave, so that one wave can finish a draw without a workgroup barrier.)
+struct Located {
+    double tot;      // the total of the masses
+    int j;           // the mass the draw falls in, or -1
+    double t_local;  // the part of u * tot inside mass j
+};
+
+__device__ __forceinline__ Located wave_locate_r(double m, double u) {
     const double incl = wave_inclusive_scan(m);
     const double tot = lane_f64(incl, kWave - 1);
     const double t = u * tot;
@@ -915,12 +922,19 @@ __device__ __forceinline__ void wave_locate(double m, double u, Smem& sm) {
     const int jc = max(j, 0);
     const double before = lane_f64(incl, max(jc - 1, 0));
     const double mj = lane_f64(m, jc);
-    if (lane == 0) {
-        sm.cross_tot = tot;
-        sm.cross = j;
-        sm.cross_t = over ? t - ((jc == 0) ? 0.0 : before) : mj;
+    return Located{tot, j, over ? t - ((jc == 0) ? 0.0 : before) : mj};
+}
+
+__device__ __forceinline__ void wave_locate(double m, double u, Smem& sm) {
+    const Located r = wave_locate_r(m, u);
+    if (threadIdx.x % kWave == 0) {
+        sm.cross_tot = r.tot;
+        sm.cross = r.j;
+        sm.cross_t = r.t_local;
     }
 }
+
+
 
 // b's decision, made once by b's decider workgroup and published as a small
 // record, one copy per reader (each mass workgroup, the draw, the bonus
@@ -989,19 +1003,188 @@ __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, in
     return d;
 }
 
+// Index (relative to rp) of the first element of target-row weights
+// w(z) = 2^(z c - kp) over n elements whose running sum exceeds t, or of the
+// last positive weight if rounding leaves the total at or below t; -1 if no
+// weight is positive.  One wave: lane l holds vectors 4 l .. 4 l + 3
+// (n <= 4 kWave E), so lane order is element order and no workgroup barrier
+// is needed.  Every lane returns the same value.
+template <class D>
+__device__ __forceinline__ int wave_find_target(const typename D::T* rp, int n, const ExactWeights& w, double t) {
+    constexpr int E = D::E;
+    constexpr int NV = 4;
+    constexpr int NE = NV * E;
+    const int lane = threadIdx.x % kWave;
+    const bool fast = (reinterpret_cast<uintptr_t>(rp) & 15u) == 0;
+    float z[NV][E], zq[NV][E];
+    load_pair_u<D, NV>(rp, rp, false, fast, lane * NV, 1, n, z, zq);
+    // the weights are recomputed where needed rather than kept (registers)
+    double sum = 0.0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < E; ++e) sum += (double)w.template eval<kTargetRow>(z[v][e], -INFINITY);
+    const double incl = wave_inclusive_scan(sum);
+    const unsigned long long over = __ballot(incl > t);
+    int mine = -1;
+    if (over) {
+        const int f = __ffsll((long long)over) - 1;
+        const double before = (f == 0) ? 0.0 : lane_f64(incl, f - 1);
+        if (lane == f) {
+            double cum = before;
+            int idx = -1, lastp = -1;
+#pragma unroll
+            for (int v = 0; v < NV; ++v)
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const float a = w.template eval<kTargetRow>(z[v][e], -INFINITY);
+                    if (a > 0.0f) lastp = v * E + e;
+                    cum += (double)a;
+                    if (idx < 0 && cum > t && a > 0.0f) idx = v * E + e;
+                }
+            if (idx < 0) idx = lastp;
+            mine = (idx >= 0) ? lane * NE + idx : -1;
+        }
+        return __builtin_amdgcn_readlane(mine, f);
+    }
+    // t lies at or beyond the total (rounding only): the last positive weight
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            if (w.template eval<kTargetRow>(z[v][e], -INFINITY) > 0.0f) mine = lane * NE + v * E + e;
+    return wave_max_int(mine);
+}
+
+// The bonus draw of b by one wave, when target row gamma has at most kWave
+// quarters (see bonus_role): the same steps as the workgroup version, with
+// every value in registers and no workgroup barrier, since this chain ends
+// the step.  The other waves of the workgroup return at once.
+template <class D, bool kRagged>
+__device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
+    using T = typename D::T;
+    if (threadIdx.x >= kWave) return;
+    const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
+    const int lane = threadIdx.x;
+    const int W = kWaves * P.nchunkg;  // quarters of the row's tiles, <= kWave
+    bool gbad;
+    const int gb = elem_gamma<kRagged>(P, b, &gbad);
+    const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gb];
+    unsigned long long* rec = P.dslot + ((size_t)b * P.ncopy + P.ncopy - 1) * kDecisionWords;
+    unsigned long long* words = P.pslot + (size_t)b * P.pstride + (size_t)2 * gamma * P.nchunk1 * 2;
+    // lane l < W: the (K, S) words of quarter l
+    const int q = min(lane, W - 1);
+    unsigned long long wk = 0ull, ws = 0ull;
+    bool ok = false;
+    for (int spin = 0;; ++spin) {
+        wk = __hip_atomic_load(words + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ws = __hip_atomic_load(words + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (__ballot(lane < W && (wk == 0ull || ws == 0ull)) == 0ull) {
+            ok = true;
+            break;
+        }
+        if (spin >= kMaxSpins) break;
+        __builtin_amdgcn_s_sleep(2);
+    }
+    // the decision copy, in flight during the draw
+    unsigned long long rw = 0ull;
+    if (lane < kDecisionWords) rw = __hip_atomic_load(rec + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // this workgroup is the only reader of these words: cleared on the way out
+    auto clear_read = [&]() {
+        if (lane < W) {
+            clear_word(words + 2 * lane);
+            clear_word(words + 2 * lane + 1);
+        }
+        if (lane < kDecisionWords) clear_word(rec + lane);
+    };
+    if (!ok) {
+        if (lane == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        clear_read();
+        return;
+    }
+    // the masses S 2^(K - Kmax) of the quarters, their total and the quarter
+    // the uniform falls in
+    const float K = (lane < W) ? (float)decode_word(wk) : -INFINITY;
+    const double S = (lane < W) ? decode_word(ws) : 0.0;
+    const float km = wave_max(K);
+    const Located loc = wave_locate_r(ldexp(S, exp_delta(K - km)), u);
+    const double total = loc.tot;
+    auto lam = [&]() { return (double)km + log2(total); };  // the row's log2-normaliser (probes only)
+    if (P.lognorm_out != nullptr && lane == 0) P.lognorm_out[(size_t)b * R + gb] = lam() * 0.693147180559945309417;
+    // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
+    int idx = -1;
+    if (isfinite(total) && total > 0.0 && loc.j >= 0) {
+        const Span sp = sub_chunk(loc.j / kWaves, loc.j % kWaves, P.chunkg, V, D::E);
+        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V + sp.begin;
+        // on the quarter's own scale 2^K: its largest weight is at least 1/2,
+        // so a quarter with positive mass has a positive fp32 weight
+        const float kj = lane_f32(K, loc.j);
+        ExactWeights w{};
+        w.kind = kTargetRow;
+        w.c = P.c;
+        w.kp = kj;
+        const int local = wave_find_target<D>(rp, sp.n, w, ldexp(loc.t_local, exp_delta(km - kj)));
+        idx = (local >= 0) ? sp.begin + local : -1;
+    }
+    // b's decision: the outputs are this workgroup's only if every draft was
+    // accepted, otherwise b's draw workgroup writes them
+    bool rok = true;
+    if (__ballot(lane < kDecisionWords && rw == 0ull) != 0ull) {
+        rok = false;
+        for (int spin = 0; spin < kMaxSpins; ++spin) {
+            __builtin_amdgcn_s_sleep(2);
+            if (lane < kDecisionWords) rw = __hip_atomic_load(rec + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (__ballot(lane < kDecisionWords && rw == 0ull) == 0ull) {
+                rok = true;
+                break;
+            }
+        }
+    }
+    clear_read();
+    if (!rok) {
+        if (lane == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const unsigned long long w0 = ~lane_u64(rw, 0);
+    const bool draw = ((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gb;
+    if (!draw) return;
+    const bool bad = idx < 0;
+    if (lane == 0) {
+        P.accepted_len[b] = bad ? -1 : gb;
+        P.next_token[b] = bad ? -1 : idx;
+        // the draw's total in units of the row normaliser (1 up to rounding)
+        if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total * exp2((double)km - lam());
+    }
+    if (P.weight_out != nullptr && !bad) {
+        // probe: p(x) over the whole row
+        ExactWeights w{};
+        w.kind = kTargetRow;
+        w.c = P.c;
+        split3(lam(), w.kp, w.lp_hi, w.lp_lo);
+        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V;
+        for (int x = lane; x < V; x += kWave)
+            P.weight_out[(size_t)b * V + x] = w.template eval<kTargetRow>(to_f32(rp[x]), -INFINITY);
+    }
+}
+
 // b's bonus workgroup (exact mode): waits for target row gamma's stats (which
 // stream last), draws the next token from that row, then reads its copy of
 // b's decision and, if every draft was accepted, writes b's outputs.  The
 // masses of the inverse-CDF draw are the sums S 2^(K - Kmax) of the row's
-// tile quarters, so the draw scans only the one quarter the uniform falls in
-// (one vector per thread).  It is the only reader of row gamma's words and
-// of its decision copy, and clears them.
+// tile quarters, so the draw scans only the one quarter the uniform falls in.
+// With at most kWave quarters one wave does all of it (bonus_wave_role);
+// otherwise the workgroup, one vector per thread.  It is the only reader of
+// row gamma's words and of its decision copy, and clears them.
 template <class D, bool kRagged>
 __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
     const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
     const int W = kWaves * P.nchunkg;  // quarters of the row's tiles
+    if (W <= kWave) {
+        bonus_wave_role<D, kRagged>(P, b);
+        return;
+    }
     bool gbad;
     const int gb = elem_gamma<kRagged>(P, b, &gbad);  // the row drawn from: target row gb
     const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gb];
@@ -1030,34 +1213,17 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
 
     // the masses S 2^(K - Kmax) of the row's chunks, their total and the chunk
     // the uniform falls in
-    float km;
-    double total, t_local;
-    int j;
-    if (W <= kWave) {
-        // one wave: a butterfly maximum and a shuffle scan, one barrier
-        if (tid < kWave) {
-            const float K = (tid < W) ? sm.K[tid] : -INFINITY;
-            const double S = (tid < W) ? sm.S[tid] : 0.0;
-            const float m0 = wave_max(K);
-            if (tid == 0) sm.kmax = m0;
-            wave_locate(ldexp(S, exp_delta(K - m0)), u, sm);
-        }
-        __syncthreads();
-        km = sm.kmax;
-        total = sm.cross_tot;
-        j = sm.cross;
-        t_local = sm.cross_t;
-    } else {
-        km = row_kmax(sm, sm.K, W);
-        for (int i = tid; i < W; i += kThreads) sm.sub[i] = ldexp(sm.S[i], exp_delta(sm.K[i] - km));
-        __syncthreads();
-        double loc[4];
-        total = mass_prefix(sm.sub, W, sm, loc);
-        t_local = 0.0;
-        j = mass_locate(sm.sub, W, u * total, loc, sm, &t_local);
-    }
-    const double lam = (double)km + log2(total);  // the row's log2-normaliser
-    if (P.lognorm_out != nullptr && tid == 0) P.lognorm_out[(size_t)b * R + gb] = lam * 0.693147180559945309417;
+    const float km = row_kmax(sm, sm.K, W);
+    for (int i = tid; i < W; i += kThreads) sm.sub[i] = ldexp(sm.S[i], exp_delta(sm.K[i] - km));
+    __syncthreads();
+    double loc[4];
+    const double total = mass_prefix(sm.sub, W, sm, loc);
+    double t_local = 0.0;
+    const int j = mass_locate(sm.sub, W, u * total, loc, sm, &t_local);
+    // the row's log2-normaliser, needed by the probe outputs only (an fp64
+    // logarithm is long on the step's last dependent chain)
+    auto lam = [&]() { return (double)km + log2(total); };
+    if (P.lognorm_out != nullptr && tid == 0) P.lognorm_out[(size_t)b * R + gb] = lam() * 0.693147180559945309417;
     // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
     int idx = -1;
     if (isfinite(total) && total > 0.0) {
@@ -1101,14 +1267,14 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
         P.accepted_len[b] = bad ? -1 : gb;
         P.next_token[b] = bad ? -1 : idx;
         // the draw's total in units of the row normaliser (1 up to rounding)
-        if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total * exp2((double)km - lam);
+        if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total * exp2((double)km - lam());
     }
     if (P.weight_out != nullptr && !bad) {
         // probe: p(x) over the whole row
         ExactWeights w{};
         w.kind = kTargetRow;
         w.c = P.c;
-        split3(lam, w.kp, w.lp_hi, w.lp_lo);
+        split3(lam(), w.kp, w.lp_hi, w.lp_lo);
         const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V;
         for (int x = tid; x < V; x += kThreads)
             P.weight_out[(size_t)b * V + x] = w.template eval<kTargetRow>(to_f32(rp[x]), -INFINITY);

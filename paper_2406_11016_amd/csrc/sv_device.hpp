@@ -162,6 +162,12 @@ __device__ __forceinline__ double lane_f64(double v, int lane) {
     return __longlong_as_double(((long long)hi << 32) | (long long)(unsigned int)lo);
 }
 
+__device__ __forceinline__ unsigned long long lane_u64(unsigned long long v, int lane) {
+    const int lo = __builtin_amdgcn_readlane((int)v, lane);
+    const int hi = __builtin_amdgcn_readlane((int)(v >> 32), lane);
+    return ((unsigned long long)(unsigned int)hi << 32) | (unsigned long long)(unsigned int)lo;
+}
+
 __device__ __forceinline__ float wave_max(float v) {
     v = fmaxf(v, dpp_f32<kDppSwap1>(v));
     v = fmaxf(v, dpp_f32<kDppSwap2>(v));
