@@ -203,6 +203,20 @@ def test_bonus_draw_over_many_row_tiles(dtype, V):
     compare(x, run_gpu(x), run_oracle(x), label=f"many row tiles {dtype}")
 
 
+@pytest.mark.parametrize("dtype,V", [("bf16", 131072), ("bf16", 131073), ("f16", 131071), ("f32", 65536),
+                                     ("f32", 65537)])
+def test_bonus_draw_at_the_one_wave_limit(dtype, V):
+    """Target row gamma in 16 tiles of 16 KiB (64 quarter masses: one wave
+    does the draw) or 17 (68: the workgroup does it), with and without a
+    ragged last tile; every draft accepted, so every element draws from that
+    row."""
+    x = W.small_case(8, 2, V, dtype, seed=95)
+    x.draft[:] = x.target[:, :2]
+    g = run_gpu(x)
+    assert np.all(g.accepted_len == 2), g.accepted_len
+    compare(x, g, run_oracle(x), label=f"one-wave limit {dtype} V={V}")
+
+
 @pytest.mark.parametrize("ab", [10.0, 1e3, 1e4, 1e5])
 def test_sigmoid_scaling_constants(ab):
     x = W.small_case(16, 10, 50272, "f16", mode="sigmoid", seed=51, temperature=0.7, alpha=-ab, beta=ab)
