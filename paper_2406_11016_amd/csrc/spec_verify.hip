@@ -9,7 +9,8 @@
 //            softmax normaliser (eq. (4)).  These move every logit byte and
 //            bound the step.
 //   decider  b: tau_c of eq. (1) at the drafted tokens and the
-//            first-rejection scan for batch element b, made once.
+//            first-rejection scan for batch element b, made once (exact
+//            mode; in the sigmoid mode every reader makes it itself).
 //   mass     (b, tile): the weights a(x) of the final distribution (residual
 //            of eqs. (2)-(3), or target row gamma) summed over the tile, one
 //            sub-chunk per wave.
@@ -439,7 +440,9 @@ __device__ int sub_chunk_find(const typename D::T* rp, const typename D::T* rq, 
 //                    quarter's normaliser terms (eq. (4)) as a (K, S) pair
 //   decider (b)      b's decision -- eq. (1) at the drafted tokens and the
 //                    first-rejection scan -- published as a small record,
-//                    one copy per reader
+//                    one copy per reader (exact mode; in the sigmoid mode
+//                    the mass and draw workgroups decide for themselves and
+//                    the decider only writes the probes)
 //   mass (b, k2)     the masses of the final distribution (eqs. (2)-(3), or
 //                    the target row) over tile k2, one per wave, published
 //   draw (b)         the inverse-CDF draw of b's next token
@@ -936,11 +939,11 @@ __device__ __forceinline__ void wave_locate(double m, double u, Smem& sm) {
 
 
 
-// b's decision, made once by b's decider workgroup and published as a small
-// record, one copy per reader (each mass workgroup, the draw, the bonus
-// workgroup), which that reader clears once it has read it.  The decider also
-// writes the tau / normaliser probes and clears the stats words it read (it
-// is their only reader).
+// b's decision, made once by b's decider workgroup and, in the exact mode,
+// published as a small record, one copy per reader (each mass workgroup, the
+// draw, the bonus workgroup), which that reader clears once it has read it.
+// The decider also writes the tau / normaliser probes and clears the stats
+// words it read (it is their only reader).
 template <class D, bool kExact, bool kRagged>
 __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& sm) {
     const int gamma = P.gamma, R = 2 * gamma + 1;
@@ -953,6 +956,8 @@ __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& s
                 ((unsigned long long)(d.gb & 0xffff) << 40),
             pack2(d.ew.kp, d.ew.lp_hi), pack2(d.ew.lp_lo, d.ew.kq), pack2(d.ew.lq_hi, d.ew.lq_lo),
             pack2(d.ew.d_hi, d.ew.d_lo)};
+        // (sigmoid mode: the mass and draw workgroups decide for themselves,
+        // so there is no record to publish; P.ncopy is 0)
         unsigned long long* dst = P.dslot + (size_t)b * P.ncopy * kDecisionWords;
         for (int i = tid; i < P.ncopy * kDecisionWords; i += kThreads) {
             const int w = i % kDecisionWords;
@@ -1281,13 +1286,24 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     }
 }
 
-template <class D, bool kExact>
+// b's decision for a mass or draw workgroup: in the exact mode the copy
+// `copy` of the decider's record; in the sigmoid mode the workgroup makes it
+// itself (eq. (5) at the 2 gamma drafted-token logits needs no row
+// normaliser, and the decision code is deterministic, so every workgroup of b
+// reaches the same one), which spares the hand-off from the decider.
+template <class D, bool kExact, bool kRagged>
+__device__ __forceinline__ Decision decision_of(const StepParams& P, int b, int copy, Smem& sm) {
+    if constexpr (kExact) return read_decision(P, b, copy, true, sm);
+    return decide<D, false, kRagged>(P, b, sm);
+}
+
+template <class D, bool kExact, bool kRagged>
 __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Smem& sm) {
     using T = typename D::T;
     constexpr int E = D::E;
     const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-    const Decision d = read_decision(P, b, k2, kExact, sm);
+    const Decision d = decision_of<D, kExact, kRagged>(P, b, k2, sm);
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     // b's bonus workgroup draws when every draft is accepted: nothing to do here
     const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == d.gb;
@@ -1308,14 +1324,14 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
 // The inverse-CDF draw for b, by b's draw workgroup, once b's mass tiles have
 // published (unless b's bonus workgroup draws); then clears b's mass words
 // for the next call.
-template <class D, bool kExact>
+template <class D, bool kExact, bool kRagged>
 __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
     constexpr int E = D::E;
     const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int M = P.nchunk2 * kWaves;
-    Decision d = read_decision(P, b, P.nchunk2, kExact, sm);
+    Decision d = decision_of<D, kExact, kRagged>(P, b, P.nchunk2, sm);
     const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == d.gb;
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (drawn) return;
@@ -1439,10 +1455,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     }
     r -= S + 1u;
     if (r < (unsigned int)Y.Mt) {
-        mass_role<D, kExact>(P, bm, (int)r, sm);
+        mass_role<D, kExact, kRagged>(P, bm, (int)r, sm);
         return;
     }
-    draw_role<D, kExact>(P, bm, sm);
+    draw_role<D, kExact, kRagged>(P, bm, sm);
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -1617,7 +1633,7 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     const bool direct = exact && pl.bonus_direct;
     P.bonus_direct = direct ? 1 : 0;
     P.nslot = exact ? (direct ? 2 * a.gamma : 2 * a.gamma + 1) : 0;
-    P.ncopy = pl.nchunk2 + (direct ? 2 : 1);
+    P.ncopy = exact ? pl.nchunk2 + (direct ? 2 : 1) : 0;
     P.pstride = (int)pl.pstride;
     const long long unit_bytes = exact ? 2LL * a.gamma * (long long)a.V * (long long)sizeof(typename D::T) : 0;
     P.y = make_layout(a.B, (long long)P.nslot * pl.nchunk1, pl.nchunk2, direct ? (long long)a.B * pl.nchunkg : 0,
