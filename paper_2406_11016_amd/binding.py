@@ -120,11 +120,19 @@ def workspace_bytes(batch: int, gamma: int, vocab: int, dtype) -> int:
 
 
 def _ptr(t: Optional[torch.Tensor]):
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+    return None if t is None else t.data_ptr()
 
 
-def _stream(device) -> ctypes.c_void_p:
-    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+# the current stream's raw handle; torch's private accessor skips building a
+# Stream object (about 2 us per call), with the public path as the fallback
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
+def _stream(device) -> int:
+    index = device.index if device.index is not None else torch.cuda.current_device()
+    if _raw_stream is not None:
+        return _raw_stream(index)
+    return torch.cuda.current_stream(device).cuda_stream
 
 
 def new_workspace(batch: int, gamma: int, vocab: int, dtype, device) -> torch.Tensor:
@@ -151,12 +159,13 @@ class Probe:
 
 
 def _validate(draft, target, tokens, uniforms):
+    dev = draft.get_device()  # -1 for host tensors
     for name, t in (("draft", draft), ("target", target), ("tokens", tokens), ("uniforms", uniforms)):
         if not t.is_cuda:
             raise SpecVerifyError(f"{name} must be a device tensor")
         if not t.is_contiguous():
             raise SpecVerifyError(f"{name} must be contiguous")
-        if t.device != draft.device:
+        if t.get_device() != dev:
             raise SpecVerifyError(f"{name} is on {t.device}, draft on {draft.device}")
     if draft.dtype not in DTYPE_CODES or target.dtype != draft.dtype:
         raise SpecVerifyError(f"logits must share one of {list(DTYPE_CODES)}; got {draft.dtype}/{target.dtype}")
@@ -186,13 +195,14 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
     """
     if mode not in ("exact", "sigmoid"):
         raise ValueError(mode)
-    lib = load_library()
+    lib = _lib if _lib is not None else load_library()
     B, g, V = _validate(draft, target, tokens, uniforms)
     dev = draft.device
+    di = draft.get_device()
     if gammas is not None:
         if probe:
             raise SpecVerifyError("the ragged variant has no probes")
-        if gammas.device != dev or gammas.dtype != torch.int32 or tuple(gammas.shape) != (B,) or \
+        if gammas.get_device() != di or gammas.dtype != torch.int32 or tuple(gammas.shape) != (B,) or \
                 not gammas.is_contiguous():
             raise SpecVerifyError(f"gammas must be a contiguous int32 [{B}] tensor on {dev}")
     if accepted_len is None:
@@ -201,11 +211,11 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
         next_token = torch.empty(B, dtype=torch.int32, device=dev)
     for name, t in (("accepted_len", accepted_len), ("next_token", next_token)):
         # the kernel writes B entries: anything else would be written out of bounds
-        if t.dtype != torch.int32 or tuple(t.shape) != (B,) or not t.is_contiguous() or t.device != dev:
+        if t.dtype != torch.int32 or tuple(t.shape) != (B,) or not t.is_contiguous() or t.get_device() != di:
             raise SpecVerifyError(f"{name} must be a contiguous int32 [{B}] tensor on {dev}")
     if workspace is None:
         workspace = new_workspace(B, g, V, draft.dtype, dev)
-    elif not workspace.is_contiguous() or workspace.device != dev:
+    elif not workspace.is_contiguous() or workspace.get_device() != di:
         raise SpecVerifyError(f"workspace must be a contiguous tensor on {dev}")
     code = DTYPE_CODES[draft.dtype]
     head = [_ptr(draft), _ptr(target), code, _ptr(tokens), _ptr(uniforms), B, g, V, float(temperature)]
