@@ -17,11 +17,14 @@
 //   draw     b: fixed-order prefix over b's sub-chunk masses, then one
 //            workgroup scan inside the sub-chunk the uniform falls in -- the
 //            inverse-CDF draw of the next token.
-//   bonus    b (exact mode): when every draft is accepted, the draw from
-//            target row gamma straight from that row's normaliser partials.
+//   bonus    b: when every draft is accepted, the draw from target row
+//            gamma straight from that row's normaliser partials (exact
+//            mode) or its sums of p_hat (sigmoid mode), prepared without
+//            waiting for the decision.
 // Sigmoid mode (eq. (5)) has no stats role: it needs no row normaliser, so
-// only the logits at the drafted tokens and the row(s) the next token is
-// drawn from are read.
+// it reads the logits at the drafted tokens, target row gamma (summed for
+// the bonus draw before the decision is known) and, after a rejection, the
+// two rows the residual is drawn from.
 #include <math.h>
 #include <stdint.h>
 
@@ -446,15 +449,19 @@ __device__ int sub_chunk_find(const typename D::T* rp, const typename D::T* rq, 
 //   mass (b, k2)     the masses of the final distribution (eqs. (2)-(3), or
 //                    the target row) over tile k2, one per wave, published
 //   draw (b)         the inverse-CDF draw of b's next token
-//   bonus (b)        exact mode: if every draft is accepted, the draw from
-//                    target row gamma straight from that row's stats sums
-//                    (no second pass over the row; see bonus_role)
+//   bonus (b)        if every draft is accepted, the draw from target row
+//                    gamma straight from that row's stats sums (exact mode;
+//                    no second pass over the row) or from its sums of p_hat
+//                    published by the sigmoid row tiles (see bonus_role)
 // Index order: units u = 0, 1, ...: unit u holds the stats tiles of the rows
 // b = u's decision reads and then b's decider (for u < B), followed by the
 // mass tiles and then the draw of b = u - lagM (for u >= lagM); then the
-// stats tiles of every target row gamma (exact mode, when the bonus role
-// draws); then the mass and draw roles of the last lagM batch elements; then
-// the bonus workgroups.  Decisions and the residual draws of most batch
+// tiles of every target row gamma (stats tiles in the exact mode, sigmoid row
+// tiles in the sigmoid mode; when the bonus role draws); then the mass and
+// draw roles of the last lagM batch elements; then the bonus workgroups.
+// (The sigmoid mode streams nothing for its decisions: its units hold only
+// the deciders, and every element's mass and draw roles come after the row
+// tiles.)  Decisions and the residual draws of most batch
 // elements so finish while the stream still runs, and the stream ends with
 // rows whose only remaining work is one scan each.
 //
@@ -504,7 +511,7 @@ struct StepParams {
     float c;                       // exact: log2(e) / T
     int chunk2, nchunk2;           // final-distribution tiles per batch element
     float s, s0;                   // sigmoid: u = fma(z, s, s0)
-    int bonus_direct;              // exact: the bonus role draws when every draft is accepted
+    int bonus_direct;              // the bonus role draws when every draft is accepted
     int nslot;                     // exact: stats slots the decider reads (2 gamma, or 2 gamma + 1)
     int ncopy;                     // copies of each decision record (one per reader)
     int pstride;                   // stats words per batch element
@@ -650,6 +657,56 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot,
         unsigned long long* out = P.pslot + (size_t)b * P.pstride + ((size_t)slot * P.nchunk1 + k) * 2;
         publish(out, (double)t.k);
         publish(out + 1, t.s);
+    }
+}
+
+// The target-row weights of a bonus draw: exact mode 2^(z c - kq) on the
+// scale of a quarter with reference kq (eq. (4) before normalisation),
+// sigmoid mode sigma(u(z)) (eq. (5), unnormalised).
+template <bool kExact>
+struct BonusWeights;
+template <>
+struct BonusWeights<true> {
+    static __device__ __forceinline__ ExactWeights of(const StepParams& P, float kq) {
+        ExactWeights w{};
+        w.kind = kTargetRow;
+        w.c = P.c;
+        w.kp = kq;
+        return w;
+    }
+};
+template <>
+struct BonusWeights<false> {
+    static __device__ __forceinline__ SigmoidWeights of(const StepParams& P, float) {
+        SigmoidWeights w{};
+        w.kind = kTargetRow;
+        w.s = P.s;
+        w.s0 = P.s0;
+        return w;
+    }
+};
+
+// Sigmoid mode, tile k of the row the next token is drawn from when every
+// draft is accepted (target row gamma, or gammas[b]): the masses
+// sum_x sigma(u(x)) of its quarters (eq. (5), unnormalised), one per wave,
+// published as pairs (0, S) in the slots of the exact mode's row-gamma pairs,
+// so that the bonus role draws from them the same way.  It waits for nothing:
+// the row needs no normaliser, so the draw need not wait for the decision.
+template <class D, bool kRagged>
+__device__ __forceinline__ void sigmoid_row_role(const StepParams& P, int b, int k) {
+    using T = typename D::T;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    bool gbad;
+    const int gb = elem_gamma<kRagged>(P, b, &gbad);
+    const T* row = static_cast<const T*>(P.target) + ((size_t)b * (P.gamma + 1) + gb) * (size_t)P.V;
+    const Span sp = sub_chunk(k, wave, P.chunkg, P.V, D::E);
+    const SigmoidWeights w = BonusWeights<false>::of(P, 0.0f);
+    const double m = (sp.n > 0) ? wave_weight_sum<D>(row + sp.begin, row + sp.begin, sp.n, w, nullptr) : 0.0;
+    if (lane == 0) {
+        unsigned long long* out =
+            P.pslot + (size_t)b * P.pstride + ((size_t)2 * P.gamma * P.nchunk1 + (size_t)k * kWaves + wave) * 2;
+        publish(out, 0.0);
+        publish(out + 1, m);
     }
 }
 
@@ -1014,8 +1071,8 @@ __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, in
 // weight is positive.  One wave: lane l holds vectors 4 l .. 4 l + 3
 // (n <= 4 kWave E), so lane order is element order and no workgroup barrier
 // is needed.  Every lane returns the same value.
-template <class D>
-__device__ __forceinline__ int wave_find_target(const typename D::T* rp, int n, const ExactWeights& w, double t) {
+template <class D, class Wt>
+__device__ __forceinline__ int wave_find_target(const typename D::T* rp, int n, const Wt& w, double t) {
     constexpr int E = D::E;
     constexpr int NV = 4;
     constexpr int NE = NV * E;
@@ -1061,11 +1118,37 @@ __device__ __forceinline__ int wave_find_target(const typename D::T* rp, int n, 
     return wave_max_int(mine);
 }
 
+// Probe outputs of a bonus draw: the draw's total (exact mode in units of the
+// row normaliser, 1 up to rounding; sigmoid mode the plain sum of p_hat) and
+// the row's weights (exact p(x), sigmoid p_hat(x)).
+template <class D, bool kExact>
+__device__ __forceinline__ void bonus_probes(const StepParams& P, int b, int gb, float km, double total, bool bad,
+                                             int t0, int nt) {
+    using T = typename D::T;
+    const int gamma = P.gamma, V = P.V;
+    auto lam = [&]() { return (double)km + log2(total); };  // exact: the row's log2-normaliser
+    if (P.mass_out != nullptr && (int)threadIdx.x == 0)
+        P.mass_out[b] = bad ? __builtin_nan("") : (kExact ? total * exp2((double)km - lam()) : total);
+    if (P.weight_out != nullptr && !bad) {
+        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V;
+        if constexpr (kExact) {
+            ExactWeights w{};
+            w.kind = kTargetRow;
+            w.c = P.c;
+            split3(lam(), w.kp, w.lp_hi, w.lp_lo);
+            for (int x = t0; x < V; x += nt) P.weight_out[(size_t)b * V + x] = w.template eval<kTargetRow>(to_f32(rp[x]), -INFINITY);
+        } else {
+            const SigmoidWeights w = BonusWeights<false>::of(P, 0.0f);
+            for (int x = t0; x < V; x += nt) P.weight_out[(size_t)b * V + x] = w.template eval<kTargetRow>(to_f32(rp[x]), -INFINITY);
+        }
+    }
+}
+
 // The bonus draw of b by one wave, when target row gamma has at most kWave
 // quarters (see bonus_role): the same steps as the workgroup version, with
 // every value in registers and no workgroup barrier, since this chain ends
 // the step.  The other waves of the workgroup return at once.
-template <class D, bool kRagged>
+template <class D, bool kExact, bool kRagged>
 __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
     using T = typename D::T;
     if (threadIdx.x >= kWave) return;
@@ -1114,8 +1197,8 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
     const float km = wave_max(K);
     const Located loc = wave_locate_r(ldexp(S, exp_delta(K - km)), u);
     const double total = loc.tot;
-    auto lam = [&]() { return (double)km + log2(total); };  // the row's log2-normaliser (probes only)
-    if (P.lognorm_out != nullptr && lane == 0) P.lognorm_out[(size_t)b * R + gb] = lam() * 0.693147180559945309417;
+    if (kExact && P.lognorm_out != nullptr && lane == 0)
+        P.lognorm_out[(size_t)b * R + gb] = ((double)km + log2(total)) * 0.693147180559945309417;
     // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
     int idx = -1;
     if (isfinite(total) && total > 0.0 && loc.j >= 0) {
@@ -1124,11 +1207,8 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
         // on the quarter's own scale 2^K: its largest weight is at least 1/2,
         // so a quarter with positive mass has a positive fp32 weight
         const float kj = lane_f32(K, loc.j);
-        ExactWeights w{};
-        w.kind = kTargetRow;
-        w.c = P.c;
-        w.kp = kj;
-        const int local = wave_find_target<D>(rp, sp.n, w, ldexp(loc.t_local, exp_delta(km - kj)));
+        const int local = wave_find_target<D>(rp, sp.n, BonusWeights<kExact>::of(P, kj),
+                                              ldexp(loc.t_local, exp_delta(km - kj)));
         idx = (local >= 0) ? sp.begin + local : -1;
     }
     // b's decision: the outputs are this workgroup's only if every draft was
@@ -1157,37 +1237,27 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
     if (lane == 0) {
         P.accepted_len[b] = bad ? -1 : gb;
         P.next_token[b] = bad ? -1 : idx;
-        // the draw's total in units of the row normaliser (1 up to rounding)
-        if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total * exp2((double)km - lam());
     }
-    if (P.weight_out != nullptr && !bad) {
-        // probe: p(x) over the whole row
-        ExactWeights w{};
-        w.kind = kTargetRow;
-        w.c = P.c;
-        split3(lam(), w.kp, w.lp_hi, w.lp_lo);
-        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V;
-        for (int x = lane; x < V; x += kWave)
-            P.weight_out[(size_t)b * V + x] = w.template eval<kTargetRow>(to_f32(rp[x]), -INFINITY);
-    }
+    bonus_probes<D, kExact>(P, b, gb, km, total, bad, lane, kWave);
 }
 
-// b's bonus workgroup (exact mode): waits for target row gamma's stats (which
-// stream last), draws the next token from that row, then reads its copy of
-// b's decision and, if every draft was accepted, writes b's outputs.  The
-// masses of the inverse-CDF draw are the sums S 2^(K - Kmax) of the row's
-// tile quarters, so the draw scans only the one quarter the uniform falls in.
+// b's bonus workgroup: waits for target row gamma's stats (exact mode; they
+// stream last) or its sigmoid row tiles (sigmoid mode), draws the next token
+// from that row, then reads its copy of b's decision and, if every draft was
+// accepted, writes b's outputs.  The masses of the inverse-CDF draw are the
+// sums S 2^(K - Kmax) of the row's tile quarters (K = 0 in the sigmoid mode),
+// so the draw scans only the one quarter the uniform falls in.
 // With at most kWave quarters one wave does all of it (bonus_wave_role);
 // otherwise the workgroup, one vector per thread.  It is the only reader of
 // row gamma's words and of its decision copy, and clears them.
-template <class D, bool kRagged>
+template <class D, bool kExact, bool kRagged>
 __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
     const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
     const int W = kWaves * P.nchunkg;  // quarters of the row's tiles
     if (W <= kWave) {
-        bonus_wave_role<D, kRagged>(P, b);
+        bonus_wave_role<D, kExact, kRagged>(P, b);
         return;
     }
     bool gbad;
@@ -1225,10 +1295,10 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     const double total = mass_prefix(sm.sub, W, sm, loc);
     double t_local = 0.0;
     const int j = mass_locate(sm.sub, W, u * total, loc, sm, &t_local);
-    // the row's log2-normaliser, needed by the probe outputs only (an fp64
-    // logarithm is long on the step's last dependent chain)
-    auto lam = [&]() { return (double)km + log2(total); };
-    if (P.lognorm_out != nullptr && tid == 0) P.lognorm_out[(size_t)b * R + gb] = lam() * 0.693147180559945309417;
+    // the row's log2-normaliser, a probe output only (an fp64 logarithm is
+    // long on the step's last dependent chain)
+    if (kExact && P.lognorm_out != nullptr && tid == 0)
+        P.lognorm_out[(size_t)b * R + gb] = ((double)km + log2(total)) * 0.693147180559945309417;
     // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
     int idx = -1;
     if (isfinite(total) && total > 0.0) {
@@ -1239,13 +1309,9 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
             const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V + begin;
             // scan on the quarter's own scale 2^K: its largest weight is at
             // least 1/2, so a quarter with positive mass has a positive weight
-            ExactWeights w{};
-            w.kind = kTargetRow;
-            w.c = P.c;
-            w.kp = sm.K[j];
             const int local = sub_chunk_find_k<D, kTargetRow, 1>(
-                rp, rp, n, w, ldexp(t_local, exp_delta(km - sm.K[j])), sm.scratch, sm.incl, sm.iscratch,
-                &sm.result);
+                rp, rp, n, BonusWeights<kExact>::of(P, sm.K[j]), ldexp(t_local, exp_delta(km - sm.K[j])),
+                sm.scratch, sm.incl, sm.iscratch, &sm.result);
             idx = (local >= 0) ? begin + local : -1;
         }
     }
@@ -1271,19 +1337,8 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     if (tid == 0) {
         P.accepted_len[b] = bad ? -1 : gb;
         P.next_token[b] = bad ? -1 : idx;
-        // the draw's total in units of the row normaliser (1 up to rounding)
-        if (P.mass_out != nullptr) P.mass_out[b] = bad ? __builtin_nan("") : total * exp2((double)km - lam());
     }
-    if (P.weight_out != nullptr && !bad) {
-        // probe: p(x) over the whole row
-        ExactWeights w{};
-        w.kind = kTargetRow;
-        w.c = P.c;
-        split3(lam(), w.kp, w.lp_hi, w.lp_lo);
-        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V;
-        for (int x = tid; x < V; x += kThreads)
-            P.weight_out[(size_t)b * V + x] = w.template eval<kTargetRow>(to_f32(rp[x]), -INFINITY);
-    }
+    bonus_probes<D, kExact>(P, b, gb, km, total, bad, tid, kThreads);
 }
 
 // b's decision for a mass or draw workgroup: in the exact mode the copy
@@ -1306,7 +1361,7 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
     const Decision d = decision_of<D, kExact, kRagged>(P, b, k2, sm);
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     // b's bonus workgroup draws when every draft is accepted: nothing to do here
-    const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == d.gb;
+    const bool drawn = P.bonus_direct && !d.bad && d.L == d.gb;
     if (drawn) return;
     const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
     double m = 0.0;
@@ -1332,7 +1387,7 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int M = P.nchunk2 * kWaves;
     Decision d = decision_of<D, kExact, kRagged>(P, b, P.nchunk2, sm);
-    const bool drawn = kExact && P.bonus_direct && !d.bad && d.L == d.gb;
+    const bool drawn = P.bonus_direct && !d.bad && d.L == d.gb;
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (drawn) return;
     unsigned long long* ms = P.mslot + (size_t)b * M;
@@ -1429,10 +1484,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         bs = Y.lagM + (int)k;
         bm = (int)k;
     } else if (id < Y.endg) {
-        // target row gamma of every batch element, streamed last
+        // target row gamma of every batch element (streamed last in the exact mode)
         const int t = (int)(id - Y.end1);
         const int b = (int)Y.dcg.of((unsigned int)t);
-        stats_role<D, kRagged>(P, b, 2 * P.gamma, t - b * P.nchunkg, sm);
+        if (kExact)
+            stats_role<D, kRagged>(P, b, 2 * P.gamma, t - b * P.nchunkg, sm);
+        else
+            sigmoid_row_role<D, kRagged>(P, b, t - b * P.nchunkg);
         return;
     } else if (id < Y.end2) {
         const unsigned int loc = id - Y.endg;
@@ -1440,7 +1498,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         r = loc - k * Y.size2 + (unsigned int)Y.S + 1u;
         bm = Y.b2 + (int)k;
     } else {
-        if (kExact) bonus_role<D, kRagged>(P, (int)(id - Y.end2), sm);
+        bonus_role<D, kExact, kRagged>(P, (int)(id - Y.end2), sm);
         return;
     }
     const unsigned int S = (unsigned int)Y.S;
@@ -1630,10 +1688,13 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.nchunkg = pl.nchunkg;
     // with the bonus role, target row gamma streams last (segment G) and the
     // deciders read the other 2 gamma rows; otherwise units hold all rows
-    const bool direct = exact && pl.bonus_direct;
+    const bool direct = pl.bonus_direct;
     P.bonus_direct = direct ? 1 : 0;
     P.nslot = exact ? (direct ? 2 * a.gamma : 2 * a.gamma + 1) : 0;
-    P.ncopy = exact ? pl.nchunk2 + (direct ? 2 : 1) : 0;
+    // decision copies: one per mass workgroup, the draw and the bonus
+    // workgroup (exact mode); only the bonus workgroup's (sigmoid mode, whose
+    // mass and draw workgroups decide for themselves)
+    P.ncopy = exact ? pl.nchunk2 + (direct ? 2 : 1) : (direct ? 1 : 0);
     P.pstride = (int)pl.pstride;
     const long long unit_bytes = exact ? 2LL * a.gamma * (long long)a.V * (long long)sizeof(typename D::T) : 0;
     P.y = make_layout(a.B, (long long)P.nslot * pl.nchunk1, pl.nchunk2, direct ? (long long)a.B * pl.nchunkg : 0,
