@@ -173,6 +173,23 @@ def test_sentinels(mode):
     assert g.accepted_len[3] == -1
 
 
+@pytest.mark.parametrize("mode", ["exact", "sigmoid"])
+def test_bad_bonus_row_leaves_a_rejecting_element_alone(mode):
+    """Target row gamma is read for the bonus draw before the decision is
+    known (in both modes); a NaN there must not touch an element that rejects
+    a draft, whose step never reads that row.  The first drafted token gets a
+    -inf target logit, so tau = 0 and it is rejected in both modes."""
+    x = W.small_case(4, 3, 700, "f32", mode=mode, seed=43, alpha=-1e3, beta=1e3)
+    for b in range(4):
+        x.target[b, 3, :] = np.nan
+        x.target[b, 0, x.tokens[b, 0]] = -np.inf
+    g = run_gpu(x)
+    o = run_oracle(x)
+    assert np.all(o.accepted_len == 0), o.accepted_len
+    assert g.accepted_len.tolist() == o.accepted_len.tolist(), (g.accepted_len, o.accepted_len)
+    compare(x, g, o, label=f"bad bonus row, rejecting {mode}")
+
+
 def test_bonus_draw_with_vanishing_leading_mass():
     """Every draft accepted and the last uniform 0: the draw takes the first
     token of positive probability.  The first 50 logits of target row gamma
