@@ -101,11 +101,12 @@ typedef enum sv_status {
  * serves both modes).  Returns 0 for invalid sizes, including vocabularies
  * above 2^20 (fp32) or 2^21 (fp16 / bf16) entries.  The workspace holds the
  * per-chunk normaliser partials (exact mode), one copy of each batch
- * element's decision per workgroup that reads it, and the per-chunk masses of
- * the final distribution.  The 32-bit word at byte offset 4 becomes nonzero
- * if a wait between workgroups ever times out (about 0.1 s), which would
- * indicate a fault; the outputs of that call are then not valid and the
- * workspace must be re-initialised.
+ * element's decision per workgroup that reads it, the per-chunk masses of
+ * the final distribution and the early exit's per-position hand-off words.
+ * The 32-bit word at byte offset 4 becomes nonzero if a wait between
+ * workgroups ever times out (about 0.1 s), which would indicate a fault; the
+ * outputs of that call are then not valid and the workspace must be
+ * re-initialised.
  */
 size_t spec_verify_workspace_bytes(int32_t batch, int32_t gamma, int32_t vocab, sv_dtype_t dtype);
 
@@ -128,6 +129,28 @@ sv_status_t spec_verify_exact(const void* draft_logits, const void* target_logit
                               int32_t batch, int32_t gamma, int32_t vocab, float temperature,
                               int32_t* accepted_len, int32_t* next_token,
                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Exact mode with an early exit: the same result as spec_verify_exact
+ * (bit-identical outputs), computed so that the logit rows a batch element
+ * does not need are mostly not read.  Sec. 3.1 stops the acceptance scan at
+ * the first rejection L, so the rows of positions after L (and target row
+ * gamma when L < gamma) play no part in the result.  The rows stream in draft
+ * order (stage c: target row c and draft row c of every batch element), each
+ * position's test of eq. (1) is made as soon as its two rows' normalisers
+ * are in, and the tiles of a stage about 56 MB of stream later (at least one
+ * stage) skip their row when their element has already rejected a draft.
+ * Worth it when B is large and drafts are often rejected; when nearly every
+ * draft is accepted it streams the same bytes as spec_verify_exact through
+ * more hand-offs.  Batches whose target row gamma is too long for the direct
+ * bonus draw (small B with a large V) run spec_verify_exact's single pass.
+ * Arguments, layout, ownership, workspace and errors as spec_verify_exact.
+ */
+sv_status_t spec_verify_exact_early_exit(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                         const int32_t* draft_tokens, const float* uniforms,
+                                         int32_t batch, int32_t gamma, int32_t vocab, float temperature,
+                                         int32_t* accepted_len, int32_t* next_token,
+                                         void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Sigmoid mode (Sec. 3.2.2, eq. (5)): p_hat = sigma((z_p / T - alpha) / (beta - alpha))

@@ -26,6 +26,7 @@ SYMBOLS = (
     "spec_verify_workspace_bytes",
     "spec_verify_workspace_init",
     "spec_verify_exact",
+    "spec_verify_exact_early_exit",
     "spec_verify_sigmoid",
     "spec_verify_exact_probe",
     "spec_verify_sigmoid_probe",
@@ -79,6 +80,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     outs = [_vp, _vp, _vp, _sz, _vp]
     lib.spec_verify_exact.argtypes = common + outs
     lib.spec_verify_exact.restype = ctypes.c_int
+    lib.spec_verify_exact_early_exit.argtypes = common + outs
+    lib.spec_verify_exact_early_exit.restype = ctypes.c_int
     lib.spec_verify_sigmoid.argtypes = common + [_f32, _f32] + outs
     lib.spec_verify_sigmoid.restype = ctypes.c_int
     lib.spec_verify_exact_probe.argtypes = common + outs + [_vp, _vp, _vp, _vp]
@@ -184,7 +187,8 @@ def _validate(draft, target, tokens, uniforms):
 def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, uniforms: torch.Tensor, *,
            mode: str = "exact", temperature: float = 1.0, alpha: float = -1.0e4, beta: float = 1.0e4,
            accepted_len: Optional[torch.Tensor] = None, next_token: Optional[torch.Tensor] = None,
-           workspace: Optional[torch.Tensor] = None, probe: bool = False, gammas: Optional[torch.Tensor] = None):
+           workspace: Optional[torch.Tensor] = None, probe: bool = False, gammas: Optional[torch.Tensor] = None,
+           early_exit: bool = False):
     """One verification step on the current stream.
 
     Returns ``(accepted_len, next_token)`` (int32 [B] device tensors), plus a
@@ -192,9 +196,14 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
     its first use) may be passed to avoid an allocation per call.  ``gammas``
     (int32 [B] device tensor) selects the ragged variant: element b uses its
     first ``gammas[b]`` drafts of the padded tensors (no probes).
+    ``early_exit`` (exact mode, no probes, not ragged) selects
+    ``spec_verify_exact_early_exit``: the same outputs, skipping most rows
+    after each element's first rejection.
     """
     if mode not in ("exact", "sigmoid"):
         raise ValueError(mode)
+    if early_exit and (mode != "exact" or probe or gammas is not None):
+        raise SpecVerifyError("the early exit is an exact-mode variant without probes or ragged gammas")
     lib = _lib if _lib is not None else load_library()
     B, g, V = _validate(draft, target, tokens, uniforms)
     dev = draft.device
@@ -241,6 +250,8 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
         if probe:
             st = lib.spec_verify_exact_probe(*head, *tail, _ptr(pr.tau), _ptr(pr.weights), _ptr(pr.mass),
                                              _ptr(pr.lognorm))
+        elif early_exit:
+            st = lib.spec_verify_exact_early_exit(*head, *tail)
         else:
             st = lib.spec_verify_exact(*head, *tail)
     else:
@@ -249,7 +260,7 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
             st = lib.spec_verify_sigmoid_probe(*head, *ab, *tail, _ptr(pr.tau), _ptr(pr.weights), _ptr(pr.mass))
         else:
             st = lib.spec_verify_sigmoid(*head, *ab, *tail)
-    _check(st, f"spec_verify_{mode}")
+    _check(st, "spec_verify_exact_early_exit" if early_exit else f"spec_verify_{mode}")
     return (accepted_len, next_token, pr) if probe else (accepted_len, next_token)
 
 

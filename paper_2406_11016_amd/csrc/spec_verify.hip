@@ -528,6 +528,11 @@ struct StepParams {
     float* weight_out;
     double* mass_out;
     double* lognorm_out;
+    // row-staged early exit (staged_kernel) only
+    unsigned long long* gslot;     // [B, gstride]: gate words of stages 0 .. gamma, then the row deciders' states
+    int gate;                      // stages s >= gate wait for the word of row decider s - gate
+    int gwords;                    // gate words per stage: max(2 nchunk1, nchunkg)
+    int gstride;                   // (gamma + 1) gwords + gamma
 };
 
 struct Smem {
@@ -717,8 +722,11 @@ __device__ __forceinline__ void sigmoid_row_role(const StepParams& P, int b, int
 // group takes pairs g, g + G, ... in order, and a DPP butterfly combines the
 // group in a fixed order, so equal rows give equal bits.  The group's first
 // lane takes the logarithm.  Ends with a workgroup barrier.
-__device__ __forceinline__ void merge_rows(Smem& sm, int R, int W) {
-    const int G = (R <= 16) ? 16 : (R <= 32) ? 8 : (R <= 64) ? 4 : (R <= 128) ? 2 : 1;
+// The group size follows from Rg if given (else R): merging fewer rows with
+// the group size of Rg rows gives each row the same bits as the larger merge.
+__device__ __forceinline__ void merge_rows(Smem& sm, int R, int W, int Rg = 0) {
+    const int Rs = (Rg > 0) ? Rg : R;
+    const int G = (Rs <= 16) ? 16 : (Rs <= 32) ? 8 : (Rs <= 64) ? 4 : (Rs <= 128) ? 2 : 1;
     const int g = threadIdx.x % G;
     for (int i0 = 0; i0 < R; i0 += kThreads / G) {
         const int i = i0 + (int)threadIdx.x / G;
@@ -1001,29 +1009,33 @@ __device__ __forceinline__ void wave_locate(double m, double u, Smem& sm) {
 // draw, the bonus workgroup), which that reader clears once it has read it.
 // The decider also writes the tau / normaliser probes and clears the stats
 // words it read (it is their only reader).
+// The P.ncopy copies of b's decision record (L, the sentinel flag, gb and the
+// residual's constants), written by every thread of the workgroup.
+__device__ __forceinline__ void publish_decision(const StepParams& P, int b, const Decision& d) {
+    const unsigned long long rec[kDecisionWords] = {
+        (unsigned long long)(d.L & 0xffff) | ((unsigned long long)(d.bad ? 1 : 0) << 16) | (1ull << 32) |
+            ((unsigned long long)(d.gb & 0xffff) << 40),
+        pack2(d.ew.kp, d.ew.lp_hi), pack2(d.ew.lp_lo, d.ew.kq), pack2(d.ew.lq_hi, d.ew.lq_lo),
+        pack2(d.ew.d_hi, d.ew.d_lo)};
+    unsigned long long* dst = P.dslot + (size_t)b * P.ncopy * kDecisionWords;
+    for (int i = threadIdx.x; i < P.ncopy * kDecisionWords; i += kThreads) {
+        const int w = i % kDecisionWords;
+        unsigned long long v = rec[0];
+#pragma unroll
+        for (int k = 1; k < kDecisionWords; ++k) v = (w == k) ? rec[k] : v;
+        publish_raw(dst + i, v);
+    }
+}
+
 template <class D, bool kExact, bool kRagged>
 __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& sm) {
     const int gamma = P.gamma, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
     const Decision d = decide<D, kExact, kRagged>(P, b, sm);
     if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    {
-        const unsigned long long rec[kDecisionWords] = {
-            (unsigned long long)(d.L & 0xffff) | ((unsigned long long)(d.bad ? 1 : 0) << 16) | (1ull << 32) |
-                ((unsigned long long)(d.gb & 0xffff) << 40),
-            pack2(d.ew.kp, d.ew.lp_hi), pack2(d.ew.lp_lo, d.ew.kq), pack2(d.ew.lq_hi, d.ew.lq_lo),
-            pack2(d.ew.d_hi, d.ew.d_lo)};
-        // (sigmoid mode: the mass and draw workgroups decide for themselves,
-        // so there is no record to publish; P.ncopy is 0)
-        unsigned long long* dst = P.dslot + (size_t)b * P.ncopy * kDecisionWords;
-        for (int i = tid; i < P.ncopy * kDecisionWords; i += kThreads) {
-            const int w = i % kDecisionWords;
-            unsigned long long v = rec[0];
-#pragma unroll
-            for (int k = 1; k < kDecisionWords; ++k) v = (w == k) ? rec[k] : v;
-            publish_raw(dst + i, v);
-        }
-    }
+    // (sigmoid mode: the mass and draw workgroups decide for themselves, so
+    // the only copy, if any, is the bonus workgroup's)
+    publish_decision(P, b, d);
     if (P.tau_out != nullptr && tid < gamma) P.tau_out[(size_t)b * gamma + tid] = sm.tau[tid];
     if (kExact) {
         const int W = P.nchunk1;
@@ -1460,6 +1472,172 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
     for (int i = tid; i < M; i += kThreads) clear_word(ms + i);
 }
 
+// ---------------------------------------------------------------------------
+// Row-staged early exit (exact mode, staged_kernel).  The decision rows of
+// every batch element stream in draft order, one stage per draft position c
+// (target row c and draft row c of every element, then target row gamma),
+// and each (b, c) has a row decider that evaluates eq. (1) at x_c as soon as
+// those two rows' normalisers are in.  The first rejection at L ends b's
+// decision: the rows of b's later stages are not needed by the method
+// (Sec. 3.1 stops at the first rejection), so a tile of stage s >= gate
+// first reads one gate word from row decider (b, s - gate) and publishes an
+// empty pair instead of streaming its row when b has already rejected a
+// draft.  The row decider that settles b (at the rejection, or at c =
+// gamma - 1 when every draft is accepted) publishes the decision record that
+// the mass, draw and bonus workgroups read, the gate words of every later
+// gated stage of b and the state words of every later row decider of b,
+// which then only consume their pairs; a row decider that accepts x_c
+// without settling b hands "running" to row decider c + 1 and "stream" to
+// the tiles of stage c + gate.  Every word still has one writer and one
+// reader, which clears it.  The merges, eq. (1) and the record are those of
+// the single-pass decider, so the outputs are bit-identical to
+// verify_kernel's.
+// ---------------------------------------------------------------------------
+enum : unsigned long long { kStateRunning = 1, kStateSettled = 2, kGateStream = 1, kGateSkip = 2 };
+
+__device__ __forceinline__ unsigned long long* gate_word(const StepParams& P, int b, int s, int j) {
+    return P.gslot + (size_t)b * P.gstride + (size_t)s * P.gwords + j;
+}
+__device__ __forceinline__ unsigned long long* state_word(const StepParams& P, int b, int c) {
+    return P.gslot + (size_t)b * P.gstride + (size_t)(P.gamma + 1) * P.gwords + c;
+}
+
+// Tile j of stage s of batch element b: for s < gamma the chunks of target
+// row s (j < nchunk1) and draft row s, for s == gamma the short tiles of
+// target row gamma.
+template <class D>
+__device__ __forceinline__ void staged_tile_role(const StepParams& P, int b, int s, int j, Smem& sm) {
+    const int gamma = P.gamma, W = P.nchunk1;
+    const int slot = (s == gamma) ? 2 * gamma : ((j < W) ? s : gamma + s);
+    const int k = (s == gamma || j < W) ? j : j - W;
+    if (s >= P.gate) {
+        unsigned long long* gw = gate_word(P, b, s, j);
+        const bool ok = wait_raw(gw, 1, sm.rec);
+        if (threadIdx.x == 0) {
+            clear_word(gw);
+            if (!ok) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (ok && sm.rec[0] == kGateSkip) {
+            // b rejected a draft at least `gate` positions earlier: an empty
+            // pair per quarter (target row gamma) or per tile, nothing read
+            const int n = (s == gamma) ? kWaves : 1;
+            const size_t first = (s == gamma) ? (size_t)slot * W + (size_t)k * kWaves : (size_t)slot * W + k;
+            if ((int)threadIdx.x < n) {
+                unsigned long long* out = P.pslot + (size_t)b * P.pstride + (first + threadIdx.x) * 2;
+                publish(out, -INFINITY);
+                publish(out + 1, 0.0);
+            }
+            return;
+        }
+    }
+    stats_role<D, false>(P, b, slot, k, sm);
+}
+
+// Row decider (b, c).
+template <class D>
+__device__ __forceinline__ void row_decider_role(const StepParams& P, int b, int c, Smem& sm) {
+    using T = typename D::T;
+    const int gamma = P.gamma, V = P.V, W = P.nchunk1;
+    const int tid = threadIdx.x;
+    const T* draft = static_cast<const T*>(P.draft) + (size_t)b * gamma * V;
+    const T* target = static_cast<const T*>(P.target) + (size_t)b * (gamma + 1) * V;
+
+    // independent loads first: every drafted token (the decider that settles
+    // b checks them all) and, in thread c, x_c's uniform and logits
+    int x = 0;
+    bool tok_ok = true;
+    double r = 0.0;
+    float zp = 0.0f, zq = 0.0f;
+    if (tid < gamma) {
+        x = P.tokens[(size_t)b * gamma + tid];
+        tok_ok = (x >= 0 && x < V);
+    }
+    if (tid == c) {
+        const int xs = tok_ok ? x : 0;
+        r = (double)P.uniforms[(size_t)b * (gamma + 1) + c];
+        zp = to_f32(target[(size_t)c * V + xs]);
+        zq = to_f32(draft[(size_t)c * V + xs]);
+    }
+
+    // the pairs of target row c (slot c) and draft row c (slot gamma + c):
+    // row 0 and row 1 of the merge
+    unsigned long long* ps = P.pslot + (size_t)b * P.pstride;
+    unsigned long long* pp = ps + (size_t)c * 2 * W;
+    unsigned long long* pq = ps + (size_t)(gamma + c) * 2 * W;
+    bool ok = poll_at<1>(4 * W, [&](int i) { return (i < 2 * W) ? pp + i : pq + (i - 2 * W); },
+                         [&](int i, unsigned long long w) {
+                             if (i & 1)
+                                 sm.S[i >> 1] = decode_word(w);
+                             else
+                                 sm.K[i >> 1] = (float)decode_word(w);
+                         });
+    for (int i = tid; i < 2 * W; i += kThreads) {
+        clear_word(pp + i);
+        clear_word(pq + i);
+    }
+    unsigned long long state = kStateRunning;
+    if (c > 0) {
+        unsigned long long* sw = state_word(P, b, c);
+        ok = wait_raw(sw, 1, sm.rec) && ok;
+        state = sm.rec[0];
+        if (tid == 0) clear_word(sw);
+    }
+    if (!ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // an earlier row decider settled b: its words for this one's successors
+    // are out already
+    if (ok && state == kStateSettled) return;
+
+    // the two rows' log2-normalisers, with the group size of the single-pass
+    // decider's 2 gamma-row merge (equal bits)
+    merge_rows(sm, 2, W, 2 * gamma);
+    if (tid == c) {
+        const double lam_p = sm.rowL[0], lam_q = sm.rowL[1];
+        const bool row_ok = isfinite(lam_p) && isfinite(lam_q);
+        double tau = 1.0;  // q(x) = 0
+        if (zq != -INFINITY) tau = min1(exp2(((double)zp - (double)zq) * (double)P.c - (lam_p - lam_q)));
+        sm.result = !row_ok ? 2 : ((r <= tau) ? 0 : 1);
+    }
+    const bool tok_bad = __syncthreads_or(!tok_ok) != 0;
+    const int stop = sm.result;
+    const bool settles = stop != 0 || c == gamma - 1 || !ok;
+    if (!settles) {
+        // x_c accepted: row decider c + 1 runs, stage c + gate streams
+        if (tid == 0) publish_raw(state_word(P, b, c + 1), kStateRunning);
+        const int s = c + P.gate;
+        if (s <= gamma) {
+            const int n = (s < gamma) ? 2 * W : P.nchunkg;
+            for (int j = tid; j < n; j += kThreads) publish_raw(gate_word(P, b, s, j), kGateStream);
+        }
+        return;
+    }
+    Decision d{};
+    d.ok = ok;
+    d.gb = gamma;
+    d.L = (stop != 0) ? c : gamma;
+    d.bad = tok_bad || stop == 2 || !ok;
+    if (!d.bad && d.L < gamma) {
+        d.ew.kind = kResidual;
+        d.ew.c = P.c;
+        split3(sm.rowL[0], d.ew.kp, d.ew.lp_hi, d.ew.lp_lo);
+        split3(sm.rowL[1], d.ew.kq, d.ew.lq_hi, d.ew.lq_lo);
+        float dummy;
+        split3(sm.rowL[0] - sm.rowL[1], d.ew.d_hi, d.ew.d_lo, dummy);
+    }
+    publish_decision(P, b, d);
+    // the later row deciders of b only consume their pairs; the later gated
+    // stages skip their rows unless every draft was accepted
+    for (int i = c + 1 + tid; i < gamma; i += kThreads) publish_raw(state_word(P, b, i), kStateSettled);
+    const unsigned long long g = (d.bad || d.L < gamma) ? kGateSkip : kGateStream;
+    const int s0 = c + P.gate;
+    if (s0 <= gamma) {
+        const int nrows = (gamma - s0) * 2 * W;  // words of stages s0 .. gamma - 1, then nchunkg of stage gamma
+        for (int i = tid; i < nrows + P.nchunkg; i += kThreads) {
+            const int s = (i < nrows) ? s0 + i / (2 * W) : gamma;
+            publish_raw(gate_word(P, b, s, (i < nrows) ? i - (s - s0) * 2 * W : i - nrows), g);
+        }
+    }
+}
+
 template <class D, bool kExact, bool kRagged>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void verify_kernel(StepParams P) {
     __shared__ Smem sm;
@@ -1519,6 +1697,45 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     draw_role<D, kExact, kRagged>(P, bm, sm);
 }
 
+// Exact mode with the row-staged early exit (see row_decider_role).  Index
+// order: units (c, b) for c = 0 .. gamma - 1, b = 0 .. B - 1, each the
+// 2 nchunk1 tiles of target row c and draft row c of b and then row decider
+// (b, c); the tiles of every target row gamma; the mass tiles and the draw of
+// every b; the bonus workgroups.  Every wait is on a smaller index: a gated
+// tile of stage s on row decider s - gate of its element (gate >= 1), a row
+// decider on its own tiles and on row decider c - 1, and the rest as in
+// verify_kernel.
+template <class D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void staged_kernel(StepParams P) {
+    __shared__ Smem sm;
+    const Layout& Y = P.y;
+    const unsigned int id = blockIdx.x;
+    if (id < Y.end0) {
+        const unsigned int u = Y.d0.of(id);  // unit c B + b
+        const unsigned int r = id - u * Y.size0;
+        const unsigned int c = Y.d1.of(u);
+        const int b = (int)(u - c * (unsigned int)P.B);
+        if (r + 1u < Y.size0)
+            staged_tile_role<D>(P, b, (int)c, (int)r, sm);
+        else
+            row_decider_role<D>(P, b, (int)c, sm);
+    } else if (id < Y.endg) {
+        const int t = (int)(id - Y.end0);
+        const int b = (int)Y.dcg.of((unsigned int)t);
+        staged_tile_role<D>(P, b, P.gamma, t - b * P.nchunkg, sm);
+    } else if (id < Y.end2) {
+        const unsigned int loc = id - Y.endg;
+        const unsigned int b = Y.d2.of(loc);
+        const unsigned int r = loc - b * Y.size2;
+        if (r < (unsigned int)Y.Mt)
+            mass_role<D, true, false>(P, (int)b, (int)r, sm);
+        else
+            draw_role<D, true, false>(P, (int)b, sm);
+    } else {
+        bonus_role<D, true, false>(P, (int)(id - Y.end2), sm);
+    }
+}
+
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
         p[i] = 0u;
@@ -1535,7 +1752,9 @@ struct Plan {
     bool bonus_direct;
     long long pstride;
     long long n_stats, n_mass;
-    size_t off_dslot, off_pslot, off_mslot, bytes;
+    int gwords;          // row-staged early exit: gate words per stage
+    long long gstride;   //                        and gate + state words per batch element
+    size_t off_dslot, off_pslot, off_mslot, off_gslot, bytes;
 };
 
 static inline long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
@@ -1599,6 +1818,10 @@ static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     off = align256(off + sizeof(unsigned long long) * (size_t)B * p->pstride);
     p->off_mslot = off;
     off = align256(off + sizeof(unsigned long long) * (size_t)p->n_mass * kWaves);
+    p->gwords = std::max(2 * p->nchunk1, p->nchunkg);
+    p->gstride = (long long)(gamma + 1) * p->gwords + gamma;
+    p->off_gslot = off;
+    off = align256(off + sizeof(unsigned long long) * (size_t)B * p->gstride);
     p->bytes = off;
     return true;
 }
@@ -1648,6 +1871,32 @@ static Layout make_layout(long long B, long long S, long long Mt, long long G, i
     return y;
 }
 
+// The row-staged layout: gamma B units of 2 nchunk1 tiles and a row decider
+// (unit c B + b), G = B nchunkg tiles of the target rows gamma, B units of Mt
+// mass tiles and a draw; the B bonus workgroups follow end2.
+static Layout make_staged_layout(long long B, long long gamma, int nchunk1, int nchunkg, long long Mt) {
+    Layout y{};
+    y.size0 = (unsigned int)(2LL * nchunk1 + 1);
+    y.size2 = (unsigned int)(Mt + 1);
+    y.end0 = (unsigned int)(gamma * B * y.size0);
+    y.end1 = y.end0;
+    y.endg = (unsigned int)(y.end0 + B * nchunkg);
+    y.end2 = (unsigned int)(y.endg + B * y.size2);
+    y.Mt = (int)Mt;
+    y.d0 = make_div(y.size0);
+    y.d1 = make_div((unsigned int)B);
+    y.d2 = make_div(y.size2);
+    y.dcg = make_div((unsigned int)std::max(1, nchunkg));
+    return y;
+}
+
+// Stages between a row decider and the tiles it gates: about kLagStreamBytes
+// of stream (the time a decision takes to publish under load), so that a
+// gated tile rarely waits.
+static int gate_stages(long long B, long long V, long long s) {
+    return (int)std::max(1LL, ceil_div(kLagStreamBytes, 2 * B * V * s));
+}
+
 struct Call {
     const void* draft;
     const void* target;
@@ -1666,6 +1915,7 @@ struct Call {
     double* mass_out;
     double* lognorm_out;
     const int32_t* gammas;  // ragged variant, else nullptr
+    bool staged = false;    // exact mode: the row-staged early exit
 };
 
 template <class D>
@@ -1716,6 +1966,20 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.weight_out = a.weight_out;
     P.mass_out = a.mass_out;
     P.lognorm_out = a.lognorm_out;
+    const long long n_staged = (long long)a.B * (a.gamma * (2LL * pl.nchunk1 + 1) + pl.nchunkg + pl.nchunk2 + 2);
+    if (exact && a.staged && direct && a.gammas == nullptr && n_staged <= 0x7fffffffLL) {
+        // the row-staged early exit (staged_kernel); without the bonus role
+        // (small batches with large vocabularies), or past 2^31 workgroups,
+        // the single pass serves (same results)
+        P.gslot = reinterpret_cast<unsigned long long*>(ws + pl.off_gslot);
+        P.gwords = pl.gwords;
+        P.gstride = (int)pl.gstride;
+        P.gate = gate_stages(a.B, a.V, (long long)sizeof(typename D::T));
+        P.y = make_staged_layout(a.B, a.gamma, pl.nchunk1, pl.nchunkg, pl.nchunk2);
+        const dim3 sgrid((unsigned int)((long long)P.y.end2 + a.B)), sblock(kThreads);
+        hipLaunchKernelGGL((staged_kernel<D>), sgrid, sblock, 0, a.stream, P);
+        return hipGetLastError() == hipSuccess ? SV_OK : SV_ERR_HIP;
+    }
     const dim3 grid((unsigned int)n_total), block(kThreads);
     if (a.gammas == nullptr) {
         if (exact)
@@ -1784,6 +2048,17 @@ sv_status_t spec_verify_exact(const void* draft_logits, const void* target_logit
     sv::Call a{draft_logits, target_logits, dtype, draft_tokens, uniforms, batch, gamma, vocab, temperature,
                0.0f, 0.0f, accepted_len, next_token, workspace, workspace_bytes, stream,
                nullptr, nullptr, nullptr, nullptr, nullptr};
+    return sv::run(a, true);
+}
+
+sv_status_t spec_verify_exact_early_exit(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                         const int32_t* draft_tokens, const float* uniforms, int32_t batch,
+                                         int32_t gamma, int32_t vocab, float temperature, int32_t* accepted_len,
+                                         int32_t* next_token, void* workspace, size_t workspace_bytes,
+                                         hipStream_t stream) {
+    sv::Call a{draft_logits, target_logits, dtype, draft_tokens, uniforms, batch, gamma, vocab, temperature,
+               0.0f, 0.0f, accepted_len, next_token, workspace, workspace_bytes, stream,
+               nullptr, nullptr, nullptr, nullptr, nullptr, true};
     return sv::run(a, true);
 }
 
