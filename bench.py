@@ -271,10 +271,12 @@ def main() -> int:
     ap.add_argument("--no-unfused", action="store_true", help="skip timing the unfused PyTorch comparison")
     ap.add_argument("--graph", choices=("auto", "on", "off"), default="auto",
                     help="also time the calls replayed from a HIP graph (auto: for workloads under 8 MB)")
-    ap.add_argument("--sweep", choices=("gamma", "alpha_beta", "top_k", "ragged", "decode_loop"), default=None,
+    ap.add_argument("--sweep", choices=("gamma", "alpha_beta", "top_k", "ragged", "early_exit", "decode_loop"),
+                    default=None,
                     help="instead of the benchmark line: one JSON line with a sweep over gamma (1..20), over "
                          "the sigmoid constants alpha = -beta, over a top-k mask of the logits, over ragged "
-                         "per-element gamma, or the decoding loop with the gamma rule (--steps iterations)")
+                         "per-element gamma, the exact mode's early exit against its single pass, or the decoding "
+                         "loop with the gamma rule (--steps iterations)")
     ap.add_argument("--copy-calibration-mb", type=float, default=0.0,
                     help="only run a plain copy of this size (for counter calibration) and exit")
     args = ap.parse_args()

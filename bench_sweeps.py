@@ -33,7 +33,8 @@ def log(msg: str) -> None:
     print(f"[sweep] {msg}", file=sys.stderr, flush=True)
 
 
-def _time_steps(w, x, steps: int, warmup: int, rotate_mb: float = 768.0, gammas=None) -> float:
+def _time_steps(w, x, steps: int, warmup: int, rotate_mb: float = 768.0, gammas=None,
+                early_exit: bool = False) -> float:
     """Microseconds per call, HIP events on the launch stream, rotating input copies."""
     import torch
 
@@ -50,7 +51,7 @@ def _time_steps(w, x, steps: int, warmup: int, rotate_mb: float = 768.0, gammas=
     def step(i):
         d, t = sets[i % nrot]
         binding.verify(d, t, tok, uni, mode=w.mode, temperature=w.temperature, alpha=w.alpha, beta=w.beta,
-                       accepted_len=acc, next_token=nxt, workspace=ws, gammas=gd)
+                       accepted_len=acc, next_token=nxt, workspace=ws, gammas=gd, early_exit=early_exit)
 
     for i in range(warmup):
         step(i)
@@ -223,6 +224,43 @@ def sweep_ragged(steps: int, warmup: int) -> dict:
     return {"sweep": "ragged", "workload": w.name, "points": points}
 
 
+def sweep_early_exit(steps: int, warmup: int) -> dict:
+    """spec_verify_exact_early_exit against spec_verify_exact on the bf16 shape
+    with the largest vocabulary (gamma = 8, V = 128,256) at B = 64 and 128, over
+    target-minus-draft noise levels that take the acceptance from ~0.97 down.
+    needed_bytes = sum_b of the rows the method uses: 2 (L_b + 1) V s when b
+    rejects at L_b, (2 gamma + 1) V s when it accepts every draft."""
+    import numpy as np
+
+    from paper_2406_11016_amd import binding
+    from paper_2406_11016_amd import workloads as W
+    head = W.WORKLOADS["exact_b64_g8_v128256_bf16"]
+    plan = [(64, "student_t3", 0.7), (64, "normal", 1.0), (64, "normal", 2.0), (64, "normal", 4.0),
+            (128, "student_t3", 0.7), (128, "normal", 2.0)]
+    points = []
+    for batch, base, noise in plan:
+        w = head.with_(batch=batch, base=base, noise_scale=noise)
+        x = W.generate(w)
+        d, t, tok, uni = binding.to_device(x, "cuda")
+        L = binding.verify(d, t, tok, uni, mode="exact")[0].cpu().numpy()
+        del d, t
+        full = w.logit_bytes
+        row = w.vocab * 2
+        needed = int(np.sum(np.where(L >= w.gamma, 2 * w.gamma + 1, 2 * (np.maximum(L, 0) + 1)))) * row
+        us_single = _time_steps(w, x, steps, warmup)
+        us_early = _time_steps(w, x, steps, warmup, early_exit=True)
+        p = {"batch": batch, "base": base, "noise": noise, "mean_accepted": round(float(L.mean()), 3),
+             "p_all_accepted": round(float((L == w.gamma).mean()), 3),
+             "us_single_pass": round(us_single, 3), "us_early_exit": round(us_early, 3),
+             "speedup": round(us_single / us_early, 4), "full_bytes": full, "needed_bytes": needed,
+             "single_frac_of_8TBs": round(full / (us_single * 1e-6) / 8e12, 4),
+             "early_needed_frac_of_8TBs": round(needed / (us_early * 1e-6) / 8e12, 4)}
+        log(json.dumps(p))
+        points.append(p)
+        del x
+    return {"sweep": "early_exit", "points": points}
+
+
 def decode_loop(iterations: int, gamma_max: int = 20, pool: int = 32) -> dict:
     """The decoding loop (gamma rule, one captured graph per gamma) on the B = 1
     workloads, against the same loop with eager calls."""
@@ -293,6 +331,8 @@ def run(kind: str, steps: int, warmup: int) -> int:
         out = sweep_top_k(steps, warmup)
     elif kind == "ragged":
         out = sweep_ragged(steps, warmup)
+    elif kind == "early_exit":
+        out = sweep_early_exit(steps, warmup)
     else:
         out = decode_loop(steps)
     out["seconds"] = round(time.perf_counter() - t0, 1)
