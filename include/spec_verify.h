@@ -137,9 +137,10 @@ sv_status_t spec_verify_exact(const void* draft_logits, const void* target_logit
  * the first rejection L, so the rows of positions after L (and target row
  * gamma when L < gamma) play no part in the result.  The rows stream in draft
  * order (stage c: target row c and draft row c of every batch element), each
- * position's test of eq. (1) is made as soon as its two rows' normalisers
- * are in, and the tiles of a stage about 56 MB of stream later (at least one
- * stage) skip their row when their element has already rejected a draft.
+ * position's test of eq. (1) is made once its two rows' normalisers are in
+ * (one stage later), and the tiles of a stage about 56 MB of stream later (at
+ * least two stages) skip their row when their element has already rejected a
+ * draft.
  * Worth it when B is large and drafts are often rejected; when nearly every
  * draft is accepted it streams the same bytes as spec_verify_exact through
  * more hand-offs.  Batches whose target row gamma is too long for the direct

@@ -1700,11 +1700,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 // Exact mode with the row-staged early exit (see row_decider_role).  Index
 // order: units (c, b) for c = 0 .. gamma - 1, b = 0 .. B - 1, each the
 // 2 nchunk1 tiles of target row c and draft row c of b and then row decider
-// (b, c); the tiles of every target row gamma; the mass tiles and the draw of
-// every b; the bonus workgroups.  Every wait is on a smaller index: a gated
-// tile of stage s on row decider s - gate of its element (gate >= 1), a row
-// decider on its own tiles and on row decider c - 1, and the rest as in
-// verify_kernel.
+// (b, c - 1) (none in the units of stage 0: a row decider runs a stage behind
+// its rows, so that it does not poll while they stream); the row deciders
+// (b, gamma - 1); the tiles of every target row gamma; the mass tiles and the
+// draw of every b; the bonus workgroups.  Every wait is on a smaller index: a
+// gated tile of stage s on row decider s - gate of its element, which sits
+// among the units of stage s - gate + 1 < s (gate >= 2); a row decider on its
+// own rows' tiles and on row decider c - 1; the rest as in verify_kernel.
 template <class D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void staged_kernel(StepParams P) {
     __shared__ Smem sm;
@@ -1717,10 +1719,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         const int b = (int)(u - c * (unsigned int)P.B);
         if (r + 1u < Y.size0)
             staged_tile_role<D>(P, b, (int)c, (int)r, sm);
-        else
-            row_decider_role<D>(P, b, (int)c, sm);
+        else if (c > 0)
+            row_decider_role<D>(P, b, (int)c - 1, sm);
+    } else if (id < Y.end1) {
+        row_decider_role<D>(P, (int)(id - Y.end0), P.gamma - 1, sm);
     } else if (id < Y.endg) {
-        const int t = (int)(id - Y.end0);
+        const int t = (int)(id - Y.end1);
         const int b = (int)Y.dcg.of((unsigned int)t);
         staged_tile_role<D>(P, b, P.gamma, t - b * P.nchunkg, sm);
     } else if (id < Y.end2) {
@@ -1872,15 +1876,16 @@ static Layout make_layout(long long B, long long S, long long Mt, long long G, i
 }
 
 // The row-staged layout: gamma B units of 2 nchunk1 tiles and a row decider
-// (unit c B + b), G = B nchunkg tiles of the target rows gamma, B units of Mt
-// mass tiles and a draw; the B bonus workgroups follow end2.
+// slot (unit c B + b), B row deciders of position gamma - 1, B nchunkg tiles
+// of the target rows gamma, B units of Mt mass tiles and a draw; the B bonus
+// workgroups follow end2.
 static Layout make_staged_layout(long long B, long long gamma, int nchunk1, int nchunkg, long long Mt) {
     Layout y{};
     y.size0 = (unsigned int)(2LL * nchunk1 + 1);
     y.size2 = (unsigned int)(Mt + 1);
     y.end0 = (unsigned int)(gamma * B * y.size0);
-    y.end1 = y.end0;
-    y.endg = (unsigned int)(y.end0 + B * nchunkg);
+    y.end1 = (unsigned int)(y.end0 + B);
+    y.endg = (unsigned int)(y.end1 + B * nchunkg);
     y.end2 = (unsigned int)(y.endg + B * y.size2);
     y.Mt = (int)Mt;
     y.d0 = make_div(y.size0);
@@ -1892,9 +1897,10 @@ static Layout make_staged_layout(long long B, long long gamma, int nchunk1, int 
 
 // Stages between a row decider and the tiles it gates: about kLagStreamBytes
 // of stream (the time a decision takes to publish under load), so that a
-// gated tile rarely waits.
+// gated tile rarely waits, and at least 2 (row decider c sits among the units
+// of stage c + 1).
 static int gate_stages(long long B, long long V, long long s) {
-    return (int)std::max(1LL, ceil_div(kLagStreamBytes, 2 * B * V * s));
+    return (int)std::max(2LL, ceil_div(kLagStreamBytes, 2 * B * V * s));
 }
 
 struct Call {
@@ -1966,7 +1972,7 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.weight_out = a.weight_out;
     P.mass_out = a.mass_out;
     P.lognorm_out = a.lognorm_out;
-    const long long n_staged = (long long)a.B * (a.gamma * (2LL * pl.nchunk1 + 1) + pl.nchunkg + pl.nchunk2 + 2);
+    const long long n_staged = (long long)a.B * (a.gamma * (2LL * pl.nchunk1 + 1) + 1 + pl.nchunkg + pl.nchunk2 + 2);
     if (exact && a.staged && direct && a.gammas == nullptr && n_staged <= 0x7fffffffLL) {
         // the row-staged early exit (staged_kernel); without the bonus role
         // (small batches with large vocabularies), or past 2^31 workgroups,
