@@ -134,6 +134,22 @@ def test_invalid_shapes_dtype_params_workspace(lib):
     assert lib.spec_verify_workspace_init(0x7004, 256, None) == SV_ERR_WORKSPACE
 
 
+def _early_exit(lib, a):
+    return lib.spec_verify_exact_early_exit(a["draft"], a["target"], a["dtype"], a["tokens"], a["uniforms"],
+                                            a["B"], a["gamma"], a["V"], a["T"], a["acc"], a["nxt"], a["ws"],
+                                            a["ws_bytes"], a["stream"])
+
+
+def test_early_exit_validates_like_the_single_pass(lib):
+    need = lib.spec_verify_workspace_bytes(2, 3, 100, 0)
+    cases = [dict(B=0), dict(gamma=0), dict(gamma=129), dict(V=0), dict(dtype=5), dict(T=0.0),
+             dict(T=float("nan")), dict(ws_bytes=need - 1), dict(ws=0x7004)]
+    cases += [{f: None} for f in ("draft", "target", "tokens", "uniforms", "acc", "nxt", "ws")]
+    for kw in cases:
+        st = _early_exit(lib, _args(**kw))
+        assert st != SV_OK and st == _exact(lib, _args(**kw)), (kw, st)
+
+
 def test_probe_entry_points_validate_too(lib):
     a = _args(B=0)
     st = lib.spec_verify_exact_probe(a["draft"], a["target"], a["dtype"], a["tokens"], a["uniforms"], a["B"],
