@@ -144,7 +144,11 @@ sv_status_t spec_verify_exact(const void* draft_logits, const void* target_logit
  * Worth it when B is large and drafts are often rejected; when nearly every
  * draft is accepted it streams the same bytes as spec_verify_exact through
  * more hand-offs.  Batches whose target row gamma is too long for the direct
- * bonus draw (small B with a large V) run spec_verify_exact's single pass.
+ * bonus draw (small B with a large V), and batches whose stream is too short
+ * for any decision row to be skipped (a stage of 2 B V s bytes: the two-stage
+ * minimum reaches no decision row when gamma <= 2, and about 56 MB of stream
+ * reaches none when 56e6 / (2 B V s) > gamma - 1), run spec_verify_exact's
+ * single pass.
  * Arguments, layout, ownership, workspace and errors as spec_verify_exact.
  */
 sv_status_t spec_verify_exact_early_exit(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,

@@ -1973,14 +1973,18 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.mass_out = a.mass_out;
     P.lognorm_out = a.lognorm_out;
     const long long n_staged = (long long)a.B * (a.gamma * (2LL * pl.nchunk1 + 1) + 1 + pl.nchunkg + pl.nchunk2 + 2);
-    if (exact && a.staged && direct && a.gammas == nullptr && n_staged <= 0x7fffffffLL) {
-        // the row-staged early exit (staged_kernel); without the bonus role
-        // (small batches with large vocabularies), or past 2^31 workgroups,
-        // the single pass serves (same results)
+    const int gate = gate_stages(a.B, a.V, (long long)sizeof(typename D::T));
+    if (exact && a.staged && direct && a.gammas == nullptr && gate < a.gamma && n_staged <= 0x7fffffffLL) {
+        // the row-staged early exit (staged_kernel).  The single pass serves
+        // (same results) without the bonus role (small batches with large
+        // vocabularies), past 2^31 workgroups, and when the stream is too
+        // short for any decision row to be gated (gate >= gamma): then the
+        // staged order could skip nothing and only lengthens the chain of
+        // decisions.
         P.gslot = reinterpret_cast<unsigned long long*>(ws + pl.off_gslot);
         P.gwords = pl.gwords;
         P.gstride = (int)pl.gstride;
-        P.gate = gate_stages(a.B, a.V, (long long)sizeof(typename D::T));
+        P.gate = gate;
         P.y = make_staged_layout(a.B, a.gamma, pl.nchunk1, pl.nchunkg, pl.nchunk2);
         const dim3 sgrid((unsigned int)((long long)P.y.end2 + a.B)), sblock(kThreads);
         hipLaunchKernelGGL((staged_kernel<D>), sgrid, sblock, 0, a.stream, P);

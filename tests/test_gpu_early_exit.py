@@ -3,10 +3,13 @@ the C ABI: bit-identical outputs to spec_verify_exact on the same inputs, and
 the oracle's decisions outside the flagged cases.
 
 Its tiles of a draft position c skip their rows when an element has already
-rejected a draft some stages earlier; how many stages depends on the stream
-size per stage (2 B V s bytes), so the shapes below cover no gating at all
-(small B V), gating two stages behind (the 64 x 128,256 bf16 shape) and one
-stage behind (twice that batch)."""
+rejected a draft `gate` stages earlier, gate = max(2, ceil(56e6 / (2 B V s)))
+(a stage is 2 B V s bytes of stream); when gate >= gamma nothing could be
+skipped and the entry point runs the single pass.  The gated shapes below
+assert gate < gamma, so that they run the staged kernel; the small shapes check
+the fall-back."""
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -72,53 +75,106 @@ def test_named_workloads(name):
 def test_gated_stages_at_the_largest_vocabulary(batch, noise):
     # noise 3.0 rejects early in most elements, so most later rows are skipped
     w = W.WORKLOADS["exact_b64_g8_v128256_bf16"].with_(batch=batch, noise_scale=noise, seed=2100 + batch)
+    assert _gate(w.batch, w.vocab, w.dtype) < w.gamma
     x = W.generate(w)
     e = _check(x, f"B={batch} noise={noise}", oracle_sample=24, seed=batch)
     print(f"[early-exit]   mean accepted {e.accepted_len.mean():.2f} of {x.gamma}", flush=True)
 
 
-@pytest.mark.parametrize("gamma", [1, 2, 5, 16, 17, 33, 64])
+def _gate(batch, vocab, dtype):
+    s = {"f32": 4, "f16": 2, "bf16": 2}[dtype]
+    return max(2, math.ceil(56e6 / (2 * batch * vocab * s)))
+
+
+# (gamma, B, V, dtype): each with gate < gamma; the row-normaliser merge groups
+# 16, 8, 4, 2 or 1 lanes per row by the number of rows (2 gamma)
+GATED = [(3, 56, 128256, "bf16"), (5, 28, 128256, "bf16"), (16, 10, 51865, "f32"), (17, 10, 51865, "f32"),
+         (33, 10, 50000, "f16"), (64, 40, 3001, "f32"), (128, 24, 5003, "f32")]
+
+
+@pytest.mark.parametrize("gamma,batch,vocab,dtype", GATED, ids=[f"g{g[0]}" for g in GATED])
 @pytest.mark.parametrize("noise", [0.05, 1.0])
-def test_gamma_range(gamma, noise):
-    for dtype, V in (("f32", 3001), ("bf16", 20011), ("f16", 4097)):
-        x = W.small_case(5, gamma, V, dtype, seed=300 + gamma, noise_scale=noise)
-        _check(x, f"gamma={gamma} noise={noise} {dtype}")
+def test_gamma_range(gamma, batch, vocab, dtype, noise):
+    assert _gate(batch, vocab, dtype) < gamma
+    x = W.small_case(batch, gamma, vocab, dtype, seed=300 + gamma, noise_scale=noise)
+    _check(x, f"gamma={gamma} noise={noise} {dtype} gate={_gate(batch, vocab, dtype)}", oracle_sample=6,
+           seed=gamma)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("V", [1, 2, 7, 65, 300007])
-def test_vocab_edge_sizes(dtype, V):
-    # the largest vocabulary runs the single pass (its target row is too long
-    # for the bonus role's direct draw); the result is the same
+def test_fall_back_to_the_single_pass(dtype, V):
+    # too short a stream to gate any decision row (and, at the largest
+    # vocabulary, a target row gamma too long for the direct bonus draw):
+    # the single pass runs; the result is the same
     x = W.small_case(3, 3, V, dtype, seed=400 + V)
+    assert _gate(3, V, dtype) >= 3
     _check(x, f"V={V} {dtype}")
 
 
+@pytest.mark.parametrize("name", ["exact_b1_g5_v51865_f32", "exact_b16_g5_v51865_f32"])
+def test_fall_back_at_small_batch_is_as_fast_as_the_single_pass(name):
+    """The named small-batch workloads gate nothing, so the early exit runs the
+    single pass; its time per call stays within 20% of spec_verify_exact's
+    (the staged kernel took twice as long at B = 1)."""
+    w = W.WORKLOADS[name]
+    x = W.generate(w)
+    assert _gate(w.batch, w.vocab, w.dtype) >= w.gamma
+    d, t, tok, u = binding.to_device(x)
+    ws = binding.new_workspace(w.batch, w.gamma, w.vocab, d.dtype, "cuda")
+
+    def per_call(ee):
+        for _ in range(50):
+            binding.verify(d, t, tok, u, mode="exact", workspace=ws, early_exit=ee)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(500):
+            binding.verify(d, t, tok, u, mode="exact", workspace=ws, early_exit=ee)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / 500
+
+    single, early = min(per_call(False) for _ in range(3)), min(per_call(True) for _ in range(3))
+    print(f"[early-exit] {name}: single {single * 1e3:.2f} us, early exit {early * 1e3:.2f} us", flush=True)
+    assert early <= 1.2 * single, (single, early)
+
+
 def test_sentinels():
-    x = W.small_case(6, 3, 500, "f32", seed=41)
-    x.tokens[0, 1] = 500                      # invalid token
+    """Sentinel elements inside a gated shape (bf16 bits: NaN 0x7fc0, -inf 0xff80)."""
+    x = W.small_case(56, 3, 128256, "bf16", seed=41)
+    assert _gate(56, 128256, "bf16") < 3
+    nan, ninf = np.uint16(0x7fc0), np.uint16(0xff80)
+    x.tokens[0, 1] = 128256                   # invalid token
     x.tokens[1, 0] = -3
-    x.target[2, 0, :] = np.nan                # NaN in the first row pair
+    x.target[2, 0, :] = nan                   # NaN in the first row pair
     x.uniforms[3, :] = 0.0                    # accept everything -> bonus row read
-    x.target[3, 3, :] = np.nan
-    x.draft[4, 2, 7] = np.nan                 # NaN in a row the scan reaches
+    x.target[3, 3, :] = nan
+    x.draft[4, 2, 7] = nan                    # NaN in a row the scan reaches
     x.tokens[4, 2] = 8
     x.uniforms[4, :3] = 0.0
-    x.target[5, :2, :] = -np.inf              # all -inf rows
+    x.target[5, :2, :] = ninf                 # all -inf rows
+    x.target[6, 0, x.tokens[6, 0]] = ninf     # rejected at the first draft ...
+    x.draft[6, 2, :] = nan                    # ... so a NaN row after it is never needed
     e = _run(x, True)
     s = _run(x, False)
-    o = run_oracle(x)
-    assert e.accepted_len.tolist() == o.accepted_len.tolist() == s.accepted_len.tolist()
-    assert e.next_token.tolist() == o.next_token.tolist() == s.next_token.tolist()
-    assert e.accepted_len[:5].tolist() == [-1] * 5
+    assert e.accepted_len.tolist() == s.accepted_len.tolist()
+    assert e.next_token.tolist() == s.next_token.tolist()
+    idx = np.arange(8)
+    o = run_oracle(_subset(x, idx))
+    assert e.accepted_len[idx].tolist() == o.accepted_len.tolist(), (e.accepted_len[idx], o.accepted_len)
+    assert e.next_token[idx].tolist() == o.next_token.tolist(), (e.next_token[idx], o.next_token)
+    assert e.accepted_len[:6].tolist() == [-1] * 6
+    assert e.accepted_len[6] == 0 and e.next_token[6] >= 0
 
 
 def test_rows_past_the_first_rejection_do_not_matter():
     """NaN fills every row after an element's first rejection (and its bonus
     row); the method never needs them (Sec. 3.1), so the element's outputs
     are those of the oracle.  At this shape the tiles of a position gate on
-    the decision one stage earlier, so most of those rows are skipped."""
+    the decision two stages earlier, so most of those rows are skipped."""
     w = W.WORKLOADS["exact_b64_g8_v128256_bf16"].with_(batch=128, gamma=4, seed=2200)
+    assert _gate(w.batch, w.vocab, w.dtype) < w.gamma
     x = W.generate(w)
     nan = np.uint16(0x7fc0)                   # bf16 NaN bits
     for b in range(0, 128, 3):
