@@ -142,6 +142,18 @@ def inverse_cdf(weights: np.ndarray, u: np.ndarray):
     return j.astype(np.int64), margin
 
 
+def acceptance_margin(r: np.ndarray, tau: np.ndarray, L: np.ndarray) -> np.ndarray:
+    """How close the examined acceptance decisions came to flipping: the
+    minimum of ``|r_c - tau_c|`` over the drafts the scan of Sec. 3.1 looks
+    at, ``c = 0 .. min(L, gamma - 1)`` (it stops at the first rejection, so
+    later drafts play no part).  ``r``, ``tau`` are [B, gamma], ``L`` is [B];
+    returns [B] (the parity bar's near-threshold flag, reading 12)."""
+    gamma = tau.shape[-1]
+    examined = np.arange(gamma)[None, :] <= L[:, None]
+    with np.errstate(invalid="ignore"):
+        return np.where(examined, np.abs(r - tau), np.inf).min(axis=-1)
+
+
 # ---------------------------------------------------------------------------
 # the whole step
 # ---------------------------------------------------------------------------
@@ -216,8 +228,7 @@ def verify(draft_logits: np.ndarray, target_logits: np.ndarray,
     bad |= (L == gamma) & ~row_ok_p[:, gamma]
 
     # margins of the examined acceptance decisions
-    examined = np.arange(gamma)[None, :] <= L[:, None]
-    acc_margin = np.where(examined, np.abs(r[:, :gamma] - tau), np.inf).min(axis=-1)
+    acc_margin = acceptance_margin(r[:, :gamma], tau, L)
 
     # the distribution of the next token, eqs. (2)-(3) or the bonus row
     bi = np.arange(B)

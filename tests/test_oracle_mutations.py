@@ -36,12 +36,26 @@ def _softmax_no_temperature_guard(w):
     return e / np.sum(e, axis=-1, keepdims=True) ** 2
 
 
+def _margin_over_all_drafts(r, tau, L):
+    with np.errstate(invalid="ignore"):
+        return np.nanmin(np.abs(r - tau), axis=-1)
+
+
+def _margin_without_reject(r, tau, L):
+    gamma = tau.shape[-1]
+    examined = np.arange(gamma)[None, :] < L[:, None]     # drops the rejected draft itself
+    with np.errstate(invalid="ignore"):
+        return np.where(examined, np.abs(r - tau), np.inf).min(axis=-1)
+
+
 MUTATIONS = {
     "residual_sign": ("max_norm", _wrong_residual_sign),
     "ratio_unclamped": ("acceptance_ratio", _no_clamp_ratio),
     "cdf_left_closed": ("inverse_cdf", _cdf_left_closed),
     "sigmoid_unscaled": ("sigmoid_approximation", _sigmoid_unscaled),
     "softmax_wrong_norm": ("softmax", _softmax_no_temperature_guard),
+    "margin_over_unexamined_drafts": ("acceptance_margin", _margin_over_all_drafts),
+    "margin_without_the_rejected_draft": ("acceptance_margin", _margin_without_reject),
 }
 
 
@@ -60,7 +74,8 @@ def _golden_failures(examples):
         ok = (int(res.accepted_len[0]) == e["accepted_len"]
               and int(res.next_token[0]) == e["next_token"]
               and all(t is None or abs(res.tau[0, c] - frac(t)) < 1e-9 for c, t in enumerate(e["tau"]))
-              and np.allclose(res.final_weights[0], [frac(v) for v in e["final"]], atol=1e-9))
+              and np.allclose(res.final_weights[0], [frac(v) for v in e["final"]], atol=1e-9)
+              and abs(res.accept_margin[0] - frac(e["accept_margin"])) < 1e-9)
         failures += 0 if ok else 1
     return failures
 

@@ -147,7 +147,7 @@ def test_inverse_cdf_never_picks_zero_mass():
 
 # --- whole steps -------------------------------------------------------------
 
-@pytest.mark.parametrize("idx", range(8))
+@pytest.mark.parametrize("idx", range(9))
 def test_golden_worked_examples(golden_examples, idx):
     ex = golden_examples[idx]
     draft, target, tokens, uniforms = example_arrays(ex)
@@ -163,6 +163,11 @@ def test_golden_worked_examples(golden_examples, idx):
     assert np.allclose(res.final_weights[0], [frac(v) for v in e["final"]], rtol=1e-12, atol=1e-15)
     assert res.mass[0] == pytest.approx(frac(e["mass"]), rel=1e-12)
     assert res.cdf_margin[0] == pytest.approx(frac(e["cdf_margin"]), rel=1e-9)
+    assert res.accept_margin[0] == pytest.approx(frac(e["accept_margin"]), rel=1e-9)
+
+
+def test_golden_examples_are_all_pinned(golden_examples):
+    assert len(golden_examples) == 9
 
 
 @pytest.mark.parametrize("mode", ["exact", "sigmoid"])
