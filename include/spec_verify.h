@@ -40,8 +40,9 @@
  * 128-bit loads.
  *
  * Ownership and concurrency.  Every pointer is owned by the caller.  The
- * library never allocates, frees, synchronises or prints.  Inputs are only
- * read; outputs and the workspace are overwritten.  A call enqueues its
+ * library never allocates device memory and never prints; only
+ * spec_verify_workspace_check and the decoding loop's step wait for the
+ * stream.  Inputs are only read; outputs and the workspace are overwritten.  A call enqueues its
  * kernels on `stream` and returns without waiting: SV_OK means "launched".
  * The workspace must be zero-filled once before its first use (for example
  * with spec_verify_workspace_init); every call leaves it zero-filled again.
@@ -61,6 +62,18 @@
  * the drafted tokens of rows 0..L and the full row(s) the next token is drawn
  * from.  Logits must satisfy |z| / T < 2.3e38 (so that z * log2(e) / T is
  * finite).
+ *
+ * Timed-out waits.  The workgroups of a launch hand results to each other
+ * through the workspace, and every such wait is bounded (about 0.1 s) so that
+ * every wave exits even if a producer never runs.  A wait that gives up sets
+ * the workspace's sticky error flag (spec_verify_workspace_check reads it),
+ * and the outputs of that call are not valid: every output is still written,
+ * with -1 or a value in its range, but an element's two outputs may come
+ * from different workgroups.  Results that arrive after their reader gave up
+ * stay in the workspace, so every later call on a workspace whose flag is set
+ * writes the sentinel -1 to every output, until the workspace is zero-filled
+ * again (spec_verify_workspace_init).  No wait times out in normal
+ * operation.
  */
 #ifndef SPEC_VERIFY_H
 #define SPEC_VERIFY_H
@@ -74,8 +87,14 @@
 extern "C" {
 #endif
 
-/* Storage type of the logits. */
-typedef enum sv_dtype {
+/* Storage type of the logits.  (In C++ the enum has the fixed underlying
+ * type int32_t, so that any value a C caller passes is a valid value of the
+ * type and is rejected by the checks instead of being undefined.) */
+typedef enum sv_dtype
+#ifdef __cplusplus
+    : int32_t
+#endif
+{
     SV_F32 = 0,   /* IEEE binary32 */
     SV_F16 = 1,   /* IEEE binary16 */
     SV_BF16 = 2   /* bfloat16 (upper half of a binary32) */
@@ -89,8 +108,11 @@ typedef enum sv_status {
     SV_ERR_PARAM = -4,      /* temperature not finite and > 0; alpha/beta not finite with alpha < beta */
     SV_ERR_WORKSPACE = -5,  /* workspace smaller than spec_verify_workspace_bytes() or not 16-byte aligned */
     SV_ERR_HIP = -6,        /* a HIP launch failed (hipGetLastError after the launches), or a HIP
-                               call of the decoding loop failed */
-    SV_ERR_ALLOC = -7       /* the decoding loop could not allocate its host object */
+                               call of the decoding loop or of spec_verify_workspace_check failed */
+    SV_ERR_ALLOC = -7,      /* the decoding loop could not allocate its host object */
+    SV_ERR_TIMEOUT = -8     /* the workspace's error flag is set: a wait between workgroups timed out
+                               (in this call or an earlier one since the workspace was zero-filled);
+                               outputs are not valid until the workspace is re-initialised */
 } sv_status_t;
 
 /* Largest number of drafted tokens per step supported by one call. */
@@ -102,11 +124,12 @@ typedef enum sv_status {
  * above 2^20 (fp32) or 2^21 (fp16 / bf16) entries.  The workspace holds the
  * per-chunk normaliser partials (exact mode), one copy of each batch
  * element's decision per workgroup that reads it, the per-chunk masses of
- * the final distribution and the early exit's per-position hand-off words.
- * The 32-bit word at byte offset 4 becomes nonzero if a wait between
- * workgroups ever times out (about 0.1 s), which would indicate a fault; the
- * outputs of that call are then not valid and the workspace must be
- * re-initialised.
+ * the final distribution and the early exit's per-position hand-off words,
+ * after a 256-byte header.  Header words (32-bit, zero in a zero-filled
+ * workspace): byte offset 4 is the sticky error flag, set when a wait between
+ * workgroups times out (see "Timed-out waits" above); byte offset 8, when
+ * nonzero, replaces the default bound on every wait by that many polls (a test
+ * hook, to force the timeout path from the host).
  */
 size_t spec_verify_workspace_bytes(int32_t batch, int32_t gamma, int32_t vocab, sv_dtype_t dtype);
 
@@ -115,6 +138,17 @@ size_t spec_verify_workspace_bytes(int32_t batch, int32_t gamma, int32_t vocab, 
  * kernel (no memset node, so the call may be captured in a graph).
  */
 sv_status_t spec_verify_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * WAITS for `stream` to finish (unlike every other call here), then reads the
+ * workspace's sticky error flag: SV_OK if it is clear, SV_ERR_TIMEOUT if a wait
+ * between workgroups timed out in a call on this workspace since it was last
+ * zero-filled (the outputs of that call and of every later one are then not
+ * valid), SV_ERR_HIP if a HIP call failed.  SV_ERR_NULL for a NULL workspace,
+ * SV_ERR_WORKSPACE if it is smaller than its 256-byte header or not 16-byte
+ * aligned.
+ */
+sv_status_t spec_verify_workspace_check(const void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Exact mode (Sec. 3.1 with the softmax of eq. (4)): softmax of every target
@@ -143,12 +177,11 @@ sv_status_t spec_verify_exact(const void* draft_logits, const void* target_logit
  * draft.
  * Worth it when B is large and drafts are often rejected; when nearly every
  * draft is accepted it streams the same bytes as spec_verify_exact through
- * more hand-offs.  Batches whose target row gamma is too long for the direct
- * bonus draw (small B with a large V), and batches whose stream is too short
- * for any decision row to be skipped (a stage of 2 B V s bytes: the two-stage
- * minimum reaches no decision row when gamma <= 2, and about 56 MB of stream
- * reaches none when 56e6 / (2 B V s) > gamma - 1), run spec_verify_exact's
- * single pass.
+ * more hand-offs.  Batches whose stream is too short for any decision row to
+ * be skipped (a stage of 2 B V s bytes: the two-stage minimum reaches no
+ * decision row when gamma <= 2, and about 56 MB of stream reaches none when
+ * 56e6 / (2 B V s) > gamma - 1), and launches past 2^31 workgroups, run
+ * spec_verify_exact's single pass.
  * Arguments, layout, ownership, workspace and errors as spec_verify_exact.
  */
 sv_status_t spec_verify_exact_early_exit(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
@@ -245,18 +278,25 @@ sv_status_t spec_verify_sigmoid_ragged(const void* draft_logits, const void* tar
  * next_token into `host_out` (pinned host memory, [2B] int32: the accepted
  * lengths, then the next tokens), WAITS for the stream to finish (the host
  * needs L to choose the next gamma and the tokens to append), and writes the
- * next gamma.  With use_graphs the step and the two copies are captured into
- * a HIP graph the first time each gamma is used and replayed afterwards.
+ * next gamma.  With use_graphs the step and the three copies are captured
+ * into a HIP graph the first time each gamma is used and replayed afterwards
+ * (on ROCm 7 replaying this one-kernel graph measured slower than launching
+ * it directly, so direct launch is the better default).
+ *
+ * After the wait the step also reads the workspace's sticky error flag (copied
+ * to pinned memory with the outputs) and returns SV_ERR_TIMEOUT, leaving
+ * *next_gamma unwritten, if it is set.
  *
  * Ownership: every pointer in the descriptor is the caller's and must stay
  * valid until spec_verify_loop_destroy; the loop allocates only its host
- * object and the graphs.  The workspace must hold
+ * object, one pinned 4-byte word for the flag (at the first step) and the
+ * graphs.  The workspace must hold
  * spec_verify_workspace_bytes(batch, g, vocab, dtype) for every g up to
  * gamma_max (zero-filled before the first iteration; each iteration leaves it
  * zero-filled).  One loop must not be stepped from two threads at once.
  * Errors: SV_ERR_NULL, SV_ERR_SHAPE, SV_ERR_PARAM (mode not 0/1, gamma out
- * of 1 .. gamma_max), SV_ERR_WORKSPACE at creation; the verification's own
- * errors and SV_ERR_HIP at a step.
+ * of 1 .. gamma_max), SV_ERR_WORKSPACE, SV_ERR_ALLOC at creation; the
+ * verification's own errors, SV_ERR_HIP and SV_ERR_TIMEOUT at a step.
  */
 typedef struct sv_loop sv_loop;
 

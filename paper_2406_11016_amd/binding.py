@@ -21,10 +21,14 @@ SV_F32, SV_F16, SV_BF16 = 0, 1, 2
 DTYPE_CODES = {torch.float32: SV_F32, torch.float16: SV_F16, torch.bfloat16: SV_BF16}
 STORAGE_TORCH_DTYPES = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 MAX_GAMMA = 128
+SV_ERR_TIMEOUT = -8
+ERROR_FLAG_OFFSET = 4     # workspace header: the sticky error flag (int32)
+SPIN_LIMIT_OFFSET = 8     # workspace header: bound on each wait in polls, 0 = default (a test hook)
 
 SYMBOLS = (
     "spec_verify_workspace_bytes",
     "spec_verify_workspace_init",
+    "spec_verify_workspace_check",
     "spec_verify_exact",
     "spec_verify_exact_early_exit",
     "spec_verify_sigmoid",
@@ -41,6 +45,10 @@ SYMBOLS = (
 
 class SpecVerifyError(RuntimeError):
     pass
+
+
+class WorkspaceTimeoutError(SpecVerifyError):
+    """The workspace's error flag is set: a wait between workgroups timed out."""
 
 
 _lib = None
@@ -76,6 +84,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.spec_verify_workspace_bytes.restype = _sz
     lib.spec_verify_workspace_init.argtypes = [_vp, _sz, _vp]
     lib.spec_verify_workspace_init.restype = ctypes.c_int
+    lib.spec_verify_workspace_check.argtypes = [_vp, _sz, _vp]
+    lib.spec_verify_workspace_check.restype = ctypes.c_int
     common = [_vp, _vp, ctypes.c_int, _vp, _vp, _i32, _i32, _i32, _f32]
     outs = [_vp, _vp, _vp, _sz, _vp]
     lib.spec_verify_exact.argtypes = common + outs
@@ -111,7 +121,8 @@ def status_string(status: int) -> str:
 
 def _check(status: int, what: str) -> None:
     if status != 0:
-        raise SpecVerifyError(f"{what}: {status_string(status)} (status {status})")
+        cls = WorkspaceTimeoutError if status == SV_ERR_TIMEOUT else SpecVerifyError
+        raise cls(f"{what}: {status_string(status)} (status {status})")
 
 
 def workspace_bytes(batch: int, gamma: int, vocab: int, dtype) -> int:
@@ -153,6 +164,14 @@ def init_workspace(ws: torch.Tensor) -> None:
            "spec_verify_workspace_init")
 
 
+def check_workspace(ws: torch.Tensor) -> None:
+    """Wait for the current stream and raise WorkspaceTimeoutError if the
+    workspace's error flag is set (spec_verify_workspace_check)."""
+    lib = load_library()
+    _check(lib.spec_verify_workspace_check(_ptr(ws), ws.numel() * ws.element_size(), _stream(ws.device)),
+           "spec_verify_workspace_check")
+
+
 @dataclass
 class Probe:
     tau: torch.Tensor          # [B, gamma] fp64
@@ -188,7 +207,7 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
            mode: str = "exact", temperature: float = 1.0, alpha: float = -1.0e4, beta: float = 1.0e4,
            accepted_len: Optional[torch.Tensor] = None, next_token: Optional[torch.Tensor] = None,
            workspace: Optional[torch.Tensor] = None, probe: bool = False, gammas: Optional[torch.Tensor] = None,
-           early_exit: bool = False):
+           early_exit: bool = False, check: bool = False):
     """One verification step on the current stream.
 
     Returns ``(accepted_len, next_token)`` (int32 [B] device tensors), plus a
@@ -198,7 +217,9 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
     first ``gammas[b]`` drafts of the padded tensors (no probes).
     ``early_exit`` (exact mode, no probes, not ragged) selects
     ``spec_verify_exact_early_exit``: the same outputs, skipping most rows
-    after each element's first rejection.
+    after each element's first rejection.  ``check`` waits for the stream
+    after the call and raises :class:`WorkspaceTimeoutError` if the
+    workspace's error flag is set (see :func:`check_workspace`).
     """
     if mode not in ("exact", "sigmoid"):
         raise ValueError(mode)
@@ -238,6 +259,8 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
         else:
             st = lib.spec_verify_sigmoid_ragged(*rhead, float(alpha), float(beta), *tail)
         _check(st, f"spec_verify_{mode}_ragged")
+        if check:
+            check_workspace(workspace)
         return accepted_len, next_token
     pr = None
     if probe:
@@ -261,6 +284,8 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
         else:
             st = lib.spec_verify_sigmoid(*head, *ab, *tail)
     _check(st, "spec_verify_exact_early_exit" if early_exit else f"spec_verify_{mode}")
+    if check:
+        check_workspace(workspace)
     return (accepted_len, next_token, pr) if probe else (accepted_len, next_token)
 
 

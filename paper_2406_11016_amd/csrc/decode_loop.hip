@@ -9,8 +9,9 @@
 // accept every draft to grow).
 //
 // Host code only: the device work is the library's verification kernel and
-// two copies.  All device and pinned buffers belong to the caller; the loop
-// object holds the descriptor and the instantiated graphs.
+// three copies.  All device and pinned buffers belong to the caller; the loop
+// object holds the descriptor, one pinned word for the workspace's error flag
+// and the instantiated graphs.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -22,14 +23,19 @@
 
 struct sv_loop {
     sv_loop_desc_t d;
+    uint32_t* flag = nullptr;          // pinned: the workspace's sticky error flag (from the first step on)
     std::vector<hipGraphExec_t> exec;  // by gamma (index 0 unused); null until first use
 };
+
+// Byte offset of the sticky error flag in the workspace header.
+constexpr size_t kErrorFlagOffset = 4;
 
 namespace {
 
 // The verification of the leading [B, gamma, V] parts of the static buffers
-// and the copy of its outputs to host_out, enqueued on the loop's stream.
-sv_status_t enqueue(const sv_loop_desc_t& d, int32_t gamma) {
+// and the copy of its outputs to host_out and of the workspace's error flag,
+// enqueued on the loop's stream.
+sv_status_t enqueue(const sv_loop_desc_t& d, uint32_t* flag, int32_t gamma) {
     sv_status_t st;
     if (d.mode == 0)
         st = spec_verify_exact(d.draft, d.target, d.dtype, d.tokens, d.uniforms, d.batch, gamma, d.vocab,
@@ -42,7 +48,9 @@ sv_status_t enqueue(const sv_loop_desc_t& d, int32_t gamma) {
     if (st != SV_OK) return st;
     const size_t n = sizeof(int32_t) * (size_t)d.batch;
     if (hipMemcpyAsync(d.host_out, d.accepted_len, n, hipMemcpyDeviceToHost, d.stream) != hipSuccess ||
-        hipMemcpyAsync(d.host_out + d.batch, d.next_token, n, hipMemcpyDeviceToHost, d.stream) != hipSuccess)
+        hipMemcpyAsync(d.host_out + d.batch, d.next_token, n, hipMemcpyDeviceToHost, d.stream) != hipSuccess ||
+        hipMemcpyAsync(flag, static_cast<const char*>(d.workspace) + kErrorFlagOffset, sizeof(uint32_t),
+                       hipMemcpyDeviceToHost, d.stream) != hipSuccess)
         return SV_ERR_HIP;
     return SV_OK;
 }
@@ -50,7 +58,7 @@ sv_status_t enqueue(const sv_loop_desc_t& d, int32_t gamma) {
 sv_status_t capture(sv_loop* loop, int32_t gamma) {
     const sv_loop_desc_t& d = loop->d;
     if (hipStreamBeginCapture(d.stream, hipStreamCaptureModeThreadLocal) != hipSuccess) return SV_ERR_HIP;
-    const sv_status_t st = enqueue(d, gamma);
+    const sv_status_t st = enqueue(d, loop->flag, gamma);
     hipGraph_t graph = nullptr;
     const hipError_t end = hipStreamEndCapture(d.stream, &graph);
     if (st != SV_OK || end != hipSuccess || graph == nullptr) {
@@ -95,6 +103,15 @@ sv_status_t spec_verify_loop_step(sv_loop* loop, int32_t gamma, int32_t* next_ga
     if (loop == nullptr || next_gamma == nullptr) return SV_ERR_NULL;
     const sv_loop_desc_t& d = loop->d;
     if (gamma < 1 || gamma > d.gamma_max) return SV_ERR_PARAM;
+    if (loop->flag == nullptr) {
+        // the pinned word the flag is copied to, allocated once (a step needs
+        // the GPU anyway; creating the loop does not)
+        void* flag = nullptr;
+        if (hipHostMalloc(&flag, sizeof(uint32_t), hipHostMallocDefault) != hipSuccess || flag == nullptr)
+            return SV_ERR_HIP;
+        loop->flag = static_cast<uint32_t*>(flag);
+    }
+    *loop->flag = 0;
     if (d.use_graphs) {
         if (loop->exec[gamma] == nullptr) {
             const sv_status_t st = capture(loop, gamma);
@@ -102,10 +119,11 @@ sv_status_t spec_verify_loop_step(sv_loop* loop, int32_t gamma, int32_t* next_ga
         }
         if (hipGraphLaunch(loop->exec[gamma], d.stream) != hipSuccess) return SV_ERR_HIP;
     } else {
-        const sv_status_t st = enqueue(d, gamma);
+        const sv_status_t st = enqueue(d, loop->flag, gamma);
         if (st != SV_OK) return st;
     }
     if (hipStreamSynchronize(d.stream) != hipSuccess) return SV_ERR_HIP;
+    if (*loop->flag != 0) return SV_ERR_TIMEOUT;
     bool all = true;
     for (int32_t b = 0; b < d.batch; ++b) all = all && d.host_out[b] == gamma;
     *next_gamma = all ? (gamma + 2 < d.gamma_max ? gamma + 2 : d.gamma_max) : (gamma > 1 ? gamma - 1 : 1);
@@ -117,6 +135,7 @@ sv_status_t spec_verify_loop_destroy(sv_loop* loop) {
     sv_status_t st = SV_OK;
     for (hipGraphExec_t e : loop->exec)
         if (e != nullptr && hipGraphExecDestroy(e) != hipSuccess) st = SV_ERR_HIP;
+    if (loop->flag != nullptr && hipHostFree(loop->flag) != hipSuccess) st = SV_ERR_HIP;
     delete loop;
     return st;
 }

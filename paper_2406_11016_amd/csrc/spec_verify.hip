@@ -38,13 +38,6 @@ namespace sv {
 
 enum : int { kResidual = 0, kTargetRow = 1 };
 
-constexpr int kWantStatsTiles = 2048;    // enough workgroups to fill 256 CUs several times
-constexpr int kWantSampleTiles = 1024;
-constexpr int kStatsTileBytes = 32768;   // at most 32 KiB of one row per stats workgroup
-constexpr long long kLagStreamBytes = 56000000;  // stream between an element's stats and its mass tiles
-constexpr int kGammaTileBytes = 16384;   // target rows gamma, streamed last: short tiles end the stream sharply
-constexpr int kSampleTileBytes = 32768;
-
 // ---------------------------------------------------------------------------
 // weights of the distribution the next token is drawn from
 // ---------------------------------------------------------------------------
@@ -183,10 +176,6 @@ __device__ __forceinline__ void load_pair_u(const typename D::T* rp, const typen
 }
 
 constexpr int kPassUnroll = 4;  // vectors in flight per lane in the weight pass
-constexpr int kMaxStatsSub = 1028;  // stats chunks of one batch element (all 2 gamma + 1 rows)
-constexpr int kMaxSub = 1024;    // sub-chunk masses of one batch element (nchunk2 * kWaves)
-constexpr int kMaxSpins = 1 << 17;  // bound on every wait (about 0.1 s), so every wave exits
-constexpr int kDecisionWords = 5;          // L and the sentinel flag, then 8 floats of weight constants
 
 // ---------------------------------------------------------------------------
 // results passed between workgroups of one launch
@@ -224,11 +213,11 @@ __device__ __forceinline__ float unpack_lo(unsigned long long w) { return __uint
 
 // Waits until the n words at p are published, handing each to take(i, w)
 // (w the raw, still inverted word).  Called by every thread; returns false
-// after kMaxSpins polls.  Each poll issues NV loads per thread before it
+// after `limit` polls.  Each poll issues NV loads per thread before it
 // looks at any (indices clamped into range), so a poll costs one memory
 // round trip for up to NV * kThreads words.
 template <int NV, class A, class F>
-__device__ __forceinline__ bool poll_at(int n, A addr, F take) {
+__device__ __forceinline__ bool poll_at(int n, A addr, F take, int limit) {
     for (int spin = 0;; ++spin) {
         int missing = 0;
         for (int i0 = 0; i0 < n; i0 += NV * kThreads) {
@@ -250,34 +239,34 @@ __device__ __forceinline__ bool poll_at(int n, A addr, F take) {
             }
         }
         if (__syncthreads_or(missing) == 0) return true;
-        if (spin >= kMaxSpins) return false;
+        if (spin >= limit) return false;
         __builtin_amdgcn_s_sleep(2);
     }
 }
 
 template <int NV, class F>
-__device__ __forceinline__ bool poll_words(unsigned long long* p, int n, F take) {
-    return poll_at<NV>(n, [&](int i) { return p + i; }, take);
+__device__ __forceinline__ bool poll_words(unsigned long long* p, int n, F take, int limit) {
+    return poll_at<NV>(n, [&](int i) { return p + i; }, take, limit);
 }
 
 // The n (<= kThreads) raw record words at p, copied to dst.
-__device__ __forceinline__ bool wait_raw(unsigned long long* p, int n, unsigned long long* dst) {
-    return poll_words<1>(p, n, [&](int i, unsigned long long w) { dst[i] = ~w; });
+__device__ __forceinline__ bool wait_raw(unsigned long long* p, int n, unsigned long long* dst, int limit) {
+    return poll_words<1>(p, n, [&](int i, unsigned long long w) { dst[i] = ~w; }, limit);
 }
 
 // The n words at p, decoded to dst (LDS).
-__device__ __forceinline__ bool wait_words(unsigned long long* p, int n, double* dst) {
-    return poll_words<4>(p, n, [&](int i, unsigned long long w) { dst[i] = decode_word(w); });
+__device__ __forceinline__ bool wait_words(unsigned long long* p, int n, double* dst, int limit) {
+    return poll_words<4>(p, n, [&](int i, unsigned long long w) { dst[i] = decode_word(w); }, limit);
 }
 
 // The n (K, S) word pairs at p, decoded to K[i] (float) and S[i] (LDS).
-__device__ __forceinline__ bool wait_ks(unsigned long long* p, int n, float* K, double* S) {
+__device__ __forceinline__ bool wait_ks(unsigned long long* p, int n, float* K, double* S, int limit) {
     return poll_words<4>(p, 2 * n, [&](int i, unsigned long long w) {
         if (i & 1)
             S[i >> 1] = decode_word(w);
         else
             K[i >> 1] = (float)decode_word(w);
-    });
+    }, limit);
 }
 
 // ---------------------------------------------------------------------------
@@ -479,27 +468,6 @@ __device__ int sub_chunk_find(const typename D::T* rp, const typename D::T* rq, 
 // of the argument block together with everything the stats role reads: a
 // stats workgroup starts its stream after a single argument fetch.
 // ---------------------------------------------------------------------------
-// n / d for 0 <= n < 2^31 as one 32 x 32 -> 64-bit multiply and a shift:
-// with L = ceil(log2 d) and m = floor(2^(31+L) / d) + 1 (< 2^32), the error of
-// n m / 2^(31+L) over n / d is below 2^-L <= 1/d, so the floor is exact.
-struct Div {
-    unsigned int m, sh;
-    __device__ __forceinline__ unsigned int of(unsigned int n) const {
-        return (unsigned int)(((unsigned long long)n * m) >> sh);
-    }
-};
-
-struct Layout {
-    Div d0, d1, d2, dc1, dcg;          // division by size0, size1, size2, nchunk1, nchunkg
-    unsigned int end0, end1;           // ends of unit segments 0 (stats + decider) and 1 (all four)
-    unsigned int endg, end2;           // ends of segment G (target rows gamma) and 2 (mass + draw)
-    unsigned int size0, size1, size2;  // workgroups per unit in segments 0, 1, 2
-    int lagM;                          // unit lag of the mass and draw roles
-    int b2;                            // batch element of the first unit of segment 2
-    int S;                             // stats tiles per unit (0 in sigmoid mode)
-    int Mt;                            // mass tiles per batch element
-};
-
 struct StepParams {
     Layout y;
     const void* draft;
@@ -511,15 +479,13 @@ struct StepParams {
     float c;                       // exact: log2(e) / T
     int chunk2, nchunk2;           // final-distribution tiles per batch element
     float s, s0;                   // sigmoid: u = fma(z, s, s0)
-    int bonus_direct;              // the bonus role draws when every draft is accepted
-    int nslot;                     // exact: stats slots the decider reads (2 gamma, or 2 gamma + 1)
     int ncopy;                     // copies of each decision record (one per reader)
     int pstride;                   // stats words per batch element
     const int32_t* tokens;
     const float* uniforms;
     const int32_t* gammas;         // ragged variant: drafts of each batch element (1 .. gamma)
     double temperature, alpha, beta;
-    unsigned int* error;           // set to 1 if a wait ever timed out
+    unsigned int* header;          // workspace header: [1] sticky error flag, [2] spin limit (0: default)
     unsigned long long* dslot;     // [B, ncopy, kDecisionWords] copies of the published decision
     unsigned long long* mslot;     // [B, nchunk2, kWaves] sub-chunk masses
     int32_t* accepted_len;
@@ -552,6 +518,21 @@ struct Smem {
     unsigned long long flags[kWaves][3];
     double cross_t, cross_tot;
 };
+
+// The workspace header: word 1 is the sticky error flag (a wait of this or an
+// earlier call on the workspace timed out), word 2 the bound on each wait in
+// polls (0: kMaxSpins; a test hook).  Both are read once per role; the flag
+// only reflects earlier calls there (a later call's outputs are sentinels
+// until the workspace is re-initialised), since the kernel boundary orders
+// them.
+__device__ __forceinline__ int spin_limit(const StepParams& P) {
+    const unsigned int v = P.header[2];
+    return (v == 0u) ? kMaxSpins : (int)min(v, (unsigned int)kMaxSpins);
+}
+__device__ __forceinline__ bool sticky_error(const StepParams& P) { return P.header[1] != 0u; }
+__device__ __forceinline__ void set_error(const StepParams& P) {
+    __hip_atomic_store(P.header + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // Stats slots of a batch element: the rows its decision reads first (target
 // rows 0 .. gamma - 1, then draft rows 0 .. gamma - 1), target row gamma last.
@@ -608,7 +589,7 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot,
             return;
         }
     }
-    const int chunk = (slot == 2 * gamma && P.bonus_direct) ? P.chunkg : P.chunk1;
+    const int chunk = (slot == 2 * gamma) ? P.chunkg : P.chunk1;
     const T* row = (r <= gamma) ? static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + r) * (size_t)V
                                 : static_cast<const T*>(P.draft) + ((size_t)b * gamma + (r - gamma - 1)) * (size_t)V;
     const Span sp = sub_chunk(k, wave, chunk, V, E);
@@ -645,7 +626,7 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot,
         load_elems_or_pad<D>(base, nfull * E, n, x[0]);
         lse_absorb_block<1, E>(st, x, c);
     }
-    if (slot == 2 * gamma && P.bonus_direct) {
+    if (slot == 2 * gamma) {
         // target row gamma: one pair per wave, so the bonus draw scans a
         // single quarter (one vector per thread)
         const Lse w = wave_lse(st);
@@ -839,8 +820,8 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
         // the stats slots the decision reads, merged into log2-normalisers
         // max K + log2(sum S 2^(K - max K)) by exact power-of-two scaling
         const int W = P.nchunk1;  // chunks per row
-        d.ok = wait_ks(P.pslot + (size_t)b * P.pstride, P.nslot * W, sm.K, sm.S);
-        merge_rows(sm, P.nslot, W);
+        d.ok = wait_ks(P.pslot + (size_t)b * P.pstride, 2 * gamma * W, sm.K, sm.S, spin_limit(P));
+        merge_rows(sm, 2 * gamma, W);
     }
 
     int stop = 0;
@@ -875,15 +856,14 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     scan_stops(stop, tok_ok, sm, &first, &first_bad, &tok_bad);
     d.L = min(first, gb);
     d.gb = gb;
-    // with the bonus role, target row gb is its business (it sentinels a
-    // non-finite row itself)
-    d.bad = gbad || tok_bad || first_bad || !d.ok ||
-            (kExact && !P.bonus_direct && d.L == gb && !isfinite(sm.rowL[2 * gamma]));
+    // target row gb is the bonus role's business (it sentinels a non-finite
+    // row itself)
+    d.bad = gbad || tok_bad || first_bad || !d.ok;
     const bool two_rows = d.L < gb;
-    if (kExact && !d.bad && (two_rows || !P.bonus_direct)) {
-        const double lp = sm.rowL[two_rows ? d.L : 2 * gamma];
-        const double lq = sm.rowL[gamma + min(d.L, gb - 1)];
-        d.ew.kind = two_rows ? kResidual : kTargetRow;
+    if (kExact && !d.bad && two_rows) {
+        const double lp = sm.rowL[d.L];
+        const double lq = sm.rowL[gamma + d.L];
+        d.ew.kind = kResidual;
         d.ew.c = P.c;
         split3(lp, d.ew.kp, d.ew.lp_hi, d.ew.lp_lo);
         split3(lq, d.ew.kq, d.ew.lq_hi, d.ew.lq_lo);
@@ -1032,7 +1012,7 @@ __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& s
     const int gamma = P.gamma, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
     const Decision d = decide<D, kExact, kRagged>(P, b, sm);
-    if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (!d.ok && tid == 0) set_error(P);
     // (sigmoid mode: the mass and draw workgroups decide for themselves, so
     // the only copy, if any, is the bonus workgroup's)
     publish_decision(P, b, d);
@@ -1040,9 +1020,9 @@ __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& s
     if (kExact) {
         const int W = P.nchunk1;
         if (P.lognorm_out != nullptr)
-            for (int i = tid; i < P.nslot; i += kThreads)
+            for (int i = tid; i < 2 * gamma; i += kThreads)
                 P.lognorm_out[(size_t)b * R + slot_row(i, gamma)] = sm.rowL[i] * 0.693147180559945309417;
-        for (int i = tid; i < 2 * P.nslot * W; i += kThreads) clear_word(P.pslot + (size_t)b * P.pstride + i);
+        for (int i = tid; i < 4 * gamma * W; i += kThreads) clear_word(P.pslot + (size_t)b * P.pstride + i);
     }
 }
 
@@ -1051,12 +1031,20 @@ __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& s
 __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, int copy, bool exact, Smem& sm) {
     Decision d{};
     unsigned long long* src = P.dslot + ((size_t)b * P.ncopy + copy) * kDecisionWords;
-    d.ok = wait_raw(src, kDecisionWords, sm.rec);
+    d.ok = wait_raw(src, kDecisionWords, sm.rec, spin_limit(P));
     if ((int)threadIdx.x < kDecisionWords) clear_word(src + threadIdx.x);
     const unsigned long long w0 = sm.rec[0];
     d.L = d.ok ? (int)(w0 & 0xffff) : 0;
     d.gb = d.ok ? (int)((w0 >> 40) & 0xffff) : P.gamma;
     d.bad = ((w0 >> 16) & 1) != 0 || !d.ok;
+    // a record from this call always has 0 <= L <= gb <= gamma; anything else
+    // is left over from a call whose wait timed out (the workspace is then
+    // dirty): a sentinel, and indices kept in range
+    if (d.gb < 1 || d.gb > P.gamma || d.L > d.gb) {
+        d.bad = true;
+        d.gb = P.gamma;
+        d.L = 0;
+    }
     const int kind = (d.L < d.gb) ? kResidual : kTargetRow;
     if (exact) {
         d.ew.kind = kind;
@@ -1172,6 +1160,8 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
     const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gb];
     unsigned long long* rec = P.dslot + ((size_t)b * P.ncopy + P.ncopy - 1) * kDecisionWords;
     unsigned long long* words = P.pslot + (size_t)b * P.pstride + (size_t)2 * gamma * P.nchunk1 * 2;
+    const int limit = spin_limit(P);
+    const bool sticky = sticky_error(P);
     // lane l < W: the (K, S) words of quarter l
     const int q = min(lane, W - 1);
     unsigned long long wk = 0ull, ws = 0ull;
@@ -1183,29 +1173,16 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
             ok = true;
             break;
         }
-        if (spin >= kMaxSpins) break;
+        if (spin >= limit) break;
         __builtin_amdgcn_s_sleep(2);
     }
     // the decision copy, in flight during the draw
     unsigned long long rw = 0ull;
     if (lane < kDecisionWords) rw = __hip_atomic_load(rec + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    // this workgroup is the only reader of these words: cleared on the way out
-    auto clear_read = [&]() {
-        if (lane < W) {
-            clear_word(words + 2 * lane);
-            clear_word(words + 2 * lane + 1);
-        }
-        if (lane < kDecisionWords) clear_word(rec + lane);
-    };
-    if (!ok) {
-        if (lane == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        clear_read();
-        return;
-    }
     // the masses S 2^(K - Kmax) of the quarters, their total and the quarter
     // the uniform falls in
-    const float K = (lane < W) ? (float)decode_word(wk) : -INFINITY;
-    const double S = (lane < W) ? decode_word(ws) : 0.0;
+    const float K = (ok && lane < W) ? (float)decode_word(wk) : -INFINITY;
+    const double S = (ok && lane < W) ? decode_word(ws) : 0.0;
     const float km = wave_max(K);
     const Located loc = wave_locate_r(ldexp(S, exp_delta(K - km)), u);
     const double total = loc.tot;
@@ -1213,7 +1190,7 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
         P.lognorm_out[(size_t)b * R + gb] = ((double)km + log2(total)) * 0.693147180559945309417;
     // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
     int idx = -1;
-    if (isfinite(total) && total > 0.0 && loc.j >= 0) {
+    if (ok && isfinite(total) && total > 0.0 && loc.j >= 0) {
         const Span sp = sub_chunk(loc.j / kWaves, loc.j % kWaves, P.chunkg, V, D::E);
         const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V + sp.begin;
         // on the quarter's own scale 2^K: its largest weight is at least 1/2,
@@ -1223,12 +1200,13 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
                                               ldexp(loc.t_local, exp_delta(km - kj)));
         idx = (local >= 0) ? sp.begin + local : -1;
     }
-    // b's decision: the outputs are this workgroup's only if every draft was
-    // accepted, otherwise b's draw workgroup writes them
+    // b's decision: the outputs are this workgroup's if every draft was
+    // accepted (otherwise b's draw workgroup writes them), and also if the
+    // decision never arrives (a timed-out wait: then they are sentinels)
     bool rok = true;
     if (__ballot(lane < kDecisionWords && rw == 0ull) != 0ull) {
         rok = false;
-        for (int spin = 0; spin < kMaxSpins; ++spin) {
+        for (int spin = 0; spin < limit; ++spin) {
             __builtin_amdgcn_s_sleep(2);
             if (lane < kDecisionWords) rw = __hip_atomic_load(rec + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (__ballot(lane < kDecisionWords && rw == 0ull) == 0ull) {
@@ -1237,15 +1215,17 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
             }
         }
     }
-    clear_read();
-    if (!rok) {
-        if (lane == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return;
+    // this workgroup is the only reader of these words: cleared on the way out
+    if (lane < W) {
+        clear_word(words + 2 * lane);
+        clear_word(words + 2 * lane + 1);
     }
+    if (lane < kDecisionWords) clear_word(rec + lane);
+    if (!(ok && rok) && lane == 0) set_error(P);
     const unsigned long long w0 = ~lane_u64(rw, 0);
-    const bool draw = ((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gb;
+    const bool draw = !rok || (((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gb);
     if (!draw) return;
-    const bool bad = idx < 0;
+    const bool bad = !(ok && rok) || sticky || idx < 0;
     if (lane == 0) {
         P.accepted_len[b] = bad ? -1 : gb;
         P.next_token[b] = bad ? -1 : idx;
@@ -1277,6 +1257,8 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + gb];
     unsigned long long* rec = P.dslot + ((size_t)b * P.ncopy + P.ncopy - 1) * kDecisionWords;
     unsigned long long* words = P.pslot + (size_t)b * P.pstride + (size_t)2 * gamma * P.nchunk1 * 2;
+    const int limit = spin_limit(P);
+    const bool sticky = sticky_error(P);
     // the row's (K, S) pairs first: the draw does not depend on the decision,
     // so it runs while b's decider may still be at work (the last elements'
     // decisions publish after the stream has ended), and the decision is read
@@ -1286,35 +1268,32 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
             sm.S[i >> 1] = decode_word(w);
         else
             sm.K[i >> 1] = (float)decode_word(w);
-    });
+    }, limit);
     for (int i = tid; i < 2 * W; i += kThreads) clear_word(words + i);
-    if (!ok) {
-        if (tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (tid < kDecisionWords) clear_word(rec + tid);
-        return;
-    }
     // a first look at the decision, in flight during the draw (it is usually
     // published by now; if not, it is polled for after the draw)
     unsigned long long rw = 0ull;
     if (tid < kDecisionWords) rw = __hip_atomic_load(rec + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
-    // the masses S 2^(K - Kmax) of the row's chunks, their total and the chunk
-    // the uniform falls in
-    const float km = row_kmax(sm, sm.K, W);
-    for (int i = tid; i < W; i += kThreads) sm.sub[i] = ldexp(sm.S[i], exp_delta(sm.K[i] - km));
-    __syncthreads();
-    double loc[4];
-    const double total = mass_prefix(sm.sub, W, sm, loc);
-    double t_local = 0.0;
-    const int j = mass_locate(sm.sub, W, u * total, loc, sm, &t_local);
-    // the row's log2-normaliser, a probe output only (an fp64 logarithm is
-    // long on the step's last dependent chain)
-    if (kExact && P.lognorm_out != nullptr && tid == 0)
-        P.lognorm_out[(size_t)b * R + gb] = ((double)km + log2(total)) * 0.693147180559945309417;
-    // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
+    float km = 0.0f;
+    double total = __builtin_nan("");
     int idx = -1;
-    if (isfinite(total) && total > 0.0) {
-        if (j >= 0) {
+    if (ok) {  // (uniform over the workgroup)
+        // the masses S 2^(K - Kmax) of the row's chunks, their total and the
+        // chunk the uniform falls in
+        km = row_kmax(sm, sm.K, W);
+        for (int i = tid; i < W; i += kThreads) sm.sub[i] = ldexp(sm.S[i], exp_delta(sm.K[i] - km));
+        __syncthreads();
+        double loc[4];
+        total = mass_prefix(sm.sub, W, sm, loc);
+        double t_local = 0.0;
+        const int j = mass_locate(sm.sub, W, u * total, loc, sm, &t_local);
+        // the row's log2-normaliser, a probe output only (an fp64 logarithm
+        // is long on the step's last dependent chain)
+        if (kExact && P.lognorm_out != nullptr && tid == 0)
+            P.lognorm_out[(size_t)b * R + gb] = ((double)km + log2(total)) * 0.693147180559945309417;
+        // a NaN logit makes the total NaN, an all -inf row makes it 0: sentinel
+        if (isfinite(total) && total > 0.0 && j >= 0) {
             const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunkg, V, D::E);
             const int begin = sp.begin;
             const int n = sp.n;
@@ -1328,24 +1307,22 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
         }
     }
     // b's decision (its copy for this workgroup, cleared once read): the
-    // outputs are this workgroup's only if every draft was accepted, otherwise
-    // b's draw workgroup writes them
+    // outputs are this workgroup's if every draft was accepted (otherwise b's
+    // draw workgroup writes them), and also if the decision never arrives (a
+    // timed-out wait: then they are sentinels)
     bool rok = true;
     if (__syncthreads_and(tid >= kDecisionWords || rw != 0ull)) {
         if (tid < kDecisionWords) sm.rec[tid] = ~rw;
         __syncthreads();
     } else {
-        rok = wait_raw(rec, kDecisionWords, sm.rec);
+        rok = wait_raw(rec, kDecisionWords, sm.rec, limit);
     }
     if (tid < kDecisionWords) clear_word(rec + tid);
-    if (!rok) {
-        if (tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return;
-    }
+    if (!(ok && rok) && tid == 0) set_error(P);
     const unsigned long long w0 = sm.rec[0];
-    const bool draw = ((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gb;
+    const bool draw = !rok || (((w0 >> 16) & 1) == 0 && (int)(w0 & 0xffff) == gb);
     if (!draw) return;
-    const bool bad = idx < 0;
+    const bool bad = !(ok && rok) || sticky || idx < 0;
     if (tid == 0) {
         P.accepted_len[b] = bad ? -1 : gb;
         P.next_token[b] = bad ? -1 : idx;
@@ -1371,9 +1348,9 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
     const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const Decision d = decision_of<D, kExact, kRagged>(P, b, k2, sm);
-    if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (!d.ok && tid == 0) set_error(P);
     // b's bonus workgroup draws when every draft is accepted: nothing to do here
-    const bool drawn = P.bonus_direct && !d.bad && d.L == d.gb;
+    const bool drawn = !d.bad && d.L == d.gb;
     if (drawn) return;
     const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
     double m = 0.0;
@@ -1398,19 +1375,21 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
     const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int M = P.nchunk2 * kWaves;
+    const bool sticky = sticky_error(P);
     Decision d = decision_of<D, kExact, kRagged>(P, b, P.nchunk2, sm);
-    const bool drawn = P.bonus_direct && !d.bad && d.L == d.gb;
-    if (!d.ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // b's bonus workgroup writes the outputs when every draft is accepted
+    const bool drawn = !d.bad && d.L == d.gb;
+    if (!d.ok && tid == 0) set_error(P);
     if (drawn) return;
     unsigned long long* ms = P.mslot + (size_t)b * M;
-    const bool got = d.ok && wait_words(ms, M, sm.sub);
-    if (d.ok && !got && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool got = d.ok && wait_words(ms, M, sm.sub, spin_limit(P));
+    if (d.ok && !got && tid == 0) set_error(P);
     const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + d.gb];
     const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V;
     const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V;
     float* wrow = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V : nullptr;
     const int L = d.L;
-    bool bad = d.bad || !got;
+    bool bad = d.bad || !got || sticky;
     int idx = -1;
     double total = __builtin_nan("");
     for (int pass = 0; pass < 2 && !bad; ++pass) {
@@ -1512,10 +1491,10 @@ __device__ __forceinline__ void staged_tile_role(const StepParams& P, int b, int
     const int k = (s == gamma || j < W) ? j : j - W;
     if (s >= P.gate) {
         unsigned long long* gw = gate_word(P, b, s, j);
-        const bool ok = wait_raw(gw, 1, sm.rec);
+        const bool ok = wait_raw(gw, 1, sm.rec, spin_limit(P));
         if (threadIdx.x == 0) {
             clear_word(gw);
-            if (!ok) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (!ok) set_error(P);
         }
         if (ok && sm.rec[0] == kGateSkip) {
             // b rejected a draft at least `gate` positions earlier: an empty
@@ -1564,28 +1543,33 @@ __device__ __forceinline__ void row_decider_role(const StepParams& P, int b, int
     unsigned long long* ps = P.pslot + (size_t)b * P.pstride;
     unsigned long long* pp = ps + (size_t)c * 2 * W;
     unsigned long long* pq = ps + (size_t)(gamma + c) * 2 * W;
+    const int limit = spin_limit(P);
     bool ok = poll_at<1>(4 * W, [&](int i) { return (i < 2 * W) ? pp + i : pq + (i - 2 * W); },
                          [&](int i, unsigned long long w) {
                              if (i & 1)
                                  sm.S[i >> 1] = decode_word(w);
                              else
                                  sm.K[i >> 1] = (float)decode_word(w);
-                         });
+                         }, limit);
     for (int i = tid; i < 2 * W; i += kThreads) {
         clear_word(pp + i);
         clear_word(pq + i);
     }
     unsigned long long state = kStateRunning;
+    bool state_ok = true;
     if (c > 0) {
         unsigned long long* sw = state_word(P, b, c);
-        ok = wait_raw(sw, 1, sm.rec) && ok;
+        state_ok = wait_raw(sw, 1, sm.rec, limit);
         state = sm.rec[0];
         if (tid == 0) clear_word(sw);
     }
-    if (!ok && tid == 0) __hip_atomic_store(P.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    // an earlier row decider settled b: its words for this one's successors
-    // are out already
-    if (ok && state == kStateSettled) return;
+    if (!(ok && state_ok) && tid == 0) set_error(P);
+    // Without the state of row decider c - 1 this one cannot know whether b is
+    // still undecided: it publishes nothing, so that b's record keeps a single
+    // writer (row decider c - 1 may still settle b; if nothing does, b's
+    // readers give up and write the sentinel).  An earlier row decider that
+    // settled b has its words for this one's successors out already.
+    if (!state_ok || state == kStateSettled) return;
 
     // the two rows' log2-normalisers, with the group size of the single-pass
     // decider's 2 gamma-row merge (equal bits)
@@ -1647,24 +1631,25 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
                  "s"(P.y.size1), "s"(P.y.size2), "s"(P.y.lagM), "s"(P.y.b2), "s"(P.y.S), "s"(P.y.Mt),
                  "s"(P.draft), "s"(P.target), "s"(P.pslot), "s"(P.B), "s"(P.gamma), "s"(P.V), "s"(P.chunk1),
                  "s"(P.nchunk1), "s"(P.chunkg), "s"(P.nchunkg), "s"(P.c));
+    // the role split of role_at (plan.hpp), spelled out so that each branch
+    // calls its role directly
     const Layout& Y = P.y;
     const unsigned int id = blockIdx.x;
-    unsigned int r;        // position in the unit, counted from its first stats tile
-    int bs = 0, bm = 0;    // batch element of the stats / decider part and of the mass / draw part
+    unsigned int r;
+    int bs = 0, bm = 0;
     if (id < Y.end0) {
-        const unsigned int k = Y.d0.of(id);
+        const unsigned int k = div_of(Y.d0, id);
         r = id - k * Y.size0;
         bs = (int)k;
     } else if (id < Y.end1) {
         const unsigned int loc = id - Y.end0;
-        const unsigned int k = Y.d1.of(loc);
+        const unsigned int k = div_of(Y.d1, loc);
         r = loc - k * Y.size1;
         bs = Y.lagM + (int)k;
         bm = (int)k;
     } else if (id < Y.endg) {
-        // target row gamma of every batch element (streamed last in the exact mode)
         const int t = (int)(id - Y.end1);
-        const int b = (int)Y.dcg.of((unsigned int)t);
+        const int b = (int)div_of(Y.dcg, (unsigned int)t);
         if (kExact)
             stats_role<D, kRagged>(P, b, 2 * P.gamma, t - b * P.nchunkg, sm);
         else
@@ -1672,7 +1657,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         return;
     } else if (id < Y.end2) {
         const unsigned int loc = id - Y.endg;
-        const unsigned int k = Y.d2.of(loc);
+        const unsigned int k = div_of(Y.d2, loc);
         r = loc - k * Y.size2 + (unsigned int)Y.S + 1u;
         bm = Y.b2 + (int)k;
     } else {
@@ -1681,7 +1666,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     }
     const unsigned int S = (unsigned int)Y.S;
     if (r < S) {
-        const int slot = (int)Y.dc1.of(r);
+        const int slot = (int)div_of(Y.dc1, r);
         stats_role<D, kRagged>(P, bs, slot, (int)r - slot * P.nchunk1, sm);
         return;
     }
@@ -1713,9 +1698,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     const Layout& Y = P.y;
     const unsigned int id = blockIdx.x;
     if (id < Y.end0) {
-        const unsigned int u = Y.d0.of(id);  // unit c B + b
+        const unsigned int u = div_of(Y.d0, id);  // unit c B + b
         const unsigned int r = id - u * Y.size0;
-        const unsigned int c = Y.d1.of(u);
+        const unsigned int c = div_of(Y.d1, u);
         const int b = (int)(u - c * (unsigned int)P.B);
         if (r + 1u < Y.size0)
             staged_tile_role<D>(P, b, (int)c, (int)r, sm);
@@ -1725,11 +1710,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         row_decider_role<D>(P, (int)(id - Y.end0), P.gamma - 1, sm);
     } else if (id < Y.endg) {
         const int t = (int)(id - Y.end1);
-        const int b = (int)Y.dcg.of((unsigned int)t);
+        const int b = (int)div_of(Y.dcg, (unsigned int)t);
         staged_tile_role<D>(P, b, P.gamma, t - b * P.nchunkg, sm);
     } else if (id < Y.end2) {
         const unsigned int loc = id - Y.endg;
-        const unsigned int b = Y.d2.of(loc);
+        const unsigned int b = div_of(Y.d2, loc);
         const unsigned int r = loc - b * Y.size2;
         if (r < (unsigned int)Y.Mt)
             mass_role<D, true, false>(P, (int)b, (int)r, sm);
@@ -1748,182 +1733,6 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-struct Plan {
-    int E;
-    int chunk1, nchunk1;
-    int chunk2, nchunk2;
-    int chunkg, nchunkg;
-    bool bonus_direct;
-    long long pstride;
-    long long n_stats, n_mass;
-    int gwords;          // row-staged early exit: gate words per stage
-    long long gstride;   //                        and gate + state words per batch element
-    size_t off_dslot, off_pslot, off_mslot, off_gslot, bytes;
-};
-
-static inline long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
-static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
-
-static bool valid_dtype(sv_dtype_t dt) { return dt == SV_F32 || dt == SV_F16 || dt == SV_BF16; }
-
-// Work decomposition; the workspace size depends only on (B, gamma, V, dtype).
-static bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* p) {
-    if (B < 1 || gamma < 1 || gamma > kMaxGamma || V < 1 || !valid_dtype(dt)) return false;
-    const int E = (dt == SV_F32) ? 4 : 8;
-    const int s = (dt == SV_F32) ? 4 : 2;
-    const long long R = 2LL * gamma + 1;
-    if ((long long)B * (gamma + 1) * (long long)V > (1LL << 40)) return false;
-    const long long min_elems = (long long)kThreads * E;
-    const long long max_cells = std::max<long long>(1, ceil_div(V, min_elems));
-
-    // row chunks: enough workgroups to fill the GPU, at most 32 KiB each (smaller
-    // tiles end the stream sooner after their dispatch, but past ~10K
-    // workgroups per launch the dispatcher, not HBM, sets the pace)
-    long long nc = ceil_div(kWantStatsTiles, B * R);
-    nc = std::max(nc, ceil_div(V, kStatsTileBytes / s));
-    nc = std::min(nc, max_cells);
-    nc = std::min(nc, std::max<long long>(1, kMaxStatsSub / R));
-    const long long chunk = ceil_div(ceil_div(V, nc), E) * E;
-    p->chunk1 = (int)chunk;
-    p->nchunk1 = (int)ceil_div(V, chunk);
-    if (R * p->nchunk1 > kMaxStatsSub) return false;
-    // target row gamma in short tiles whose quarters fit the bonus role's scan
-    // (one vector per thread); the quarters' masses must fit kMaxSub
-    const long long ncg = std::max(ceil_div(V, kGammaTileBytes / s), ceil_div(V, (long long)kWaves * kThreads * E));
-    const long long chunkg = ceil_div(ceil_div(V, ncg), E) * E;
-    p->chunkg = (int)chunkg;
-    p->nchunkg = (int)ceil_div(V, chunkg);
-    p->bonus_direct = (long long)p->nchunkg * kWaves <= kMaxSub && ceil_div(chunkg / E, kWaves) <= kThreads;
-
-    // final-distribution tiles: a sub-chunk (a quarter tile) must fit one
-    // vector per thread, and b's sub-chunk masses must fit kMaxSub
-    const long long max_tile_vecs = (long long)kWaves * kThreads;
-    long long nc2 = ceil_div(kWantSampleTiles, B);
-    nc2 = std::max(nc2, ceil_div(V, kSampleTileBytes / s));
-    nc2 = std::min(nc2, max_cells);
-    nc2 = std::min(nc2, (long long)kMaxSub / kWaves);
-    nc2 = std::max(nc2, ceil_div(V, max_tile_vecs * E));
-    const long long chunk2 = ceil_div(ceil_div(V, nc2), E) * E;
-    p->chunk2 = (int)chunk2;
-    p->nchunk2 = (int)ceil_div(V, chunk2);
-    if ((long long)p->nchunk2 * kWaves > kMaxSub || chunk2 / E > max_tile_vecs) return false;
-    p->E = E;
-
-    p->n_stats = (long long)B * (2LL * gamma * p->nchunk1 + (p->bonus_direct ? p->nchunkg : p->nchunk1));
-    p->n_mass = (long long)B * p->nchunk2;
-    // plus a decider and a draw per batch element
-    if (p->n_stats + p->n_mass + 3LL * B > 0x7fffffffLL) return false;
-
-    size_t off = 256;  // header: the error flag at byte offset 4
-    p->off_dslot = off;
-    off = align256(off + sizeof(unsigned long long) * (size_t)B * (p->nchunk2 + 2) * kDecisionWords);
-    p->off_pslot = off;
-    p->pstride = 2 * (2LL * gamma * p->nchunk1 + (p->bonus_direct ? (long long)kWaves * p->nchunkg : p->nchunk1));
-    off = align256(off + sizeof(unsigned long long) * (size_t)B * p->pstride);
-    p->off_mslot = off;
-    off = align256(off + sizeof(unsigned long long) * (size_t)p->n_mass * kWaves);
-    p->gwords = std::max(2 * p->nchunk1, p->nchunkg);
-    p->gstride = (long long)(gamma + 1) * p->gwords + gamma;
-    p->off_gslot = off;
-    off = align256(off + sizeof(unsigned long long) * (size_t)B * p->gstride);
-    p->bytes = off;
-    return true;
-}
-
-// The layout for B batch elements: units with S stats tiles, a decider, Mt
-// mass tiles and a draw each; G stats tiles of the target rows gamma; Bd bonus
-// workgroups.  The mass and draw roles of b sit lagM units after its stats
-// (1 <= lagM <= B, see lag_units): late enough that b's decision is usually
-// published when they start (a waiting workgroup holds a dispatch slot the
-// stream needs), early enough that most batch elements finish within the
-// stream.
-// The lag in units: about kLagStreamBytes of stream (~9 us at 6.5 TB/s, the
-// time a decision takes to publish under load) behind the element's stats,
-// and all of them after the stream when the whole stream is shorter than
-// that (or absent: the sigmoid mode streams no rows).
-static long long lag_units(long long B, long long unit_bytes) {
-    if (unit_bytes <= 0) return B;
-    return std::min(B, std::max(1LL, ceil_div(kLagStreamBytes, unit_bytes)));
-}
-
-static Div make_div(unsigned int d) {
-    unsigned int L = 0;
-    while ((1ull << L) < d) ++L;
-    const unsigned long long m = ((1ull << (31 + L)) / d) + 1;
-    return Div{(unsigned int)m, 31 + L};
-}
-
-static Layout make_layout(long long B, long long S, long long Mt, long long G, int nchunk1, int nchunkg,
-                          long long lagM) {
-    Layout y{};
-    y.size0 = (unsigned int)(S + 1);
-    y.size1 = (unsigned int)(S + Mt + 2);
-    y.size2 = (unsigned int)(Mt + 1);
-    y.end0 = (unsigned int)(lagM * (S + 1));
-    y.end1 = (unsigned int)(y.end0 + (B - lagM) * (S + Mt + 2));
-    y.endg = (unsigned int)(y.end1 + G);
-    y.end2 = (unsigned int)(y.endg + lagM * (Mt + 1));
-    y.lagM = (int)lagM;
-    y.b2 = (int)(B - lagM);
-    y.S = (int)S;
-    y.Mt = (int)Mt;
-    y.d0 = make_div(y.size0);
-    y.d1 = make_div(y.size1);
-    y.d2 = make_div(y.size2);
-    y.dc1 = make_div((unsigned int)std::max(1, nchunk1));
-    y.dcg = make_div((unsigned int)std::max(1, nchunkg));
-    return y;
-}
-
-// The row-staged layout: gamma B units of 2 nchunk1 tiles and a row decider
-// slot (unit c B + b), B row deciders of position gamma - 1, B nchunkg tiles
-// of the target rows gamma, B units of Mt mass tiles and a draw; the B bonus
-// workgroups follow end2.
-static Layout make_staged_layout(long long B, long long gamma, int nchunk1, int nchunkg, long long Mt) {
-    Layout y{};
-    y.size0 = (unsigned int)(2LL * nchunk1 + 1);
-    y.size2 = (unsigned int)(Mt + 1);
-    y.end0 = (unsigned int)(gamma * B * y.size0);
-    y.end1 = (unsigned int)(y.end0 + B);
-    y.endg = (unsigned int)(y.end1 + B * nchunkg);
-    y.end2 = (unsigned int)(y.endg + B * y.size2);
-    y.Mt = (int)Mt;
-    y.d0 = make_div(y.size0);
-    y.d1 = make_div((unsigned int)B);
-    y.d2 = make_div(y.size2);
-    y.dcg = make_div((unsigned int)std::max(1, nchunkg));
-    return y;
-}
-
-// Stages between a row decider and the tiles it gates: about kLagStreamBytes
-// of stream (the time a decision takes to publish under load), so that a
-// gated tile rarely waits, and at least 2 (row decider c sits among the units
-// of stage c + 1).
-static int gate_stages(long long B, long long V, long long s) {
-    return (int)std::max(2LL, ceil_div(kLagStreamBytes, 2 * B * V * s));
-}
-
-struct Call {
-    const void* draft;
-    const void* target;
-    sv_dtype_t dt;
-    const int32_t* tokens;
-    const float* uniforms;
-    int32_t B, gamma, V;
-    float temperature, alpha, beta;
-    int32_t* accepted_len;
-    int32_t* next_token;
-    void* ws;
-    size_t ws_bytes;
-    hipStream_t stream;
-    double* tau_out;
-    float* weight_out;
-    double* mass_out;
-    double* lognorm_out;
-    const int32_t* gammas;  // ragged variant, else nullptr
-    bool staged = false;    // exact mode: the row-staged early exit
-};
-
 template <class D>
 static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     char* ws = static_cast<char*>(a.ws);
@@ -1942,27 +1751,17 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.nchunk2 = pl.nchunk2;
     P.chunkg = pl.chunkg;
     P.nchunkg = pl.nchunkg;
-    // with the bonus role, target row gamma streams last (segment G) and the
-    // deciders read the other 2 gamma rows; otherwise units hold all rows
-    const bool direct = pl.bonus_direct;
-    P.bonus_direct = direct ? 1 : 0;
-    P.nslot = exact ? (direct ? 2 * a.gamma : 2 * a.gamma + 1) : 0;
-    // decision copies: one per mass workgroup, the draw and the bonus
-    // workgroup (exact mode); only the bonus workgroup's (sigmoid mode, whose
-    // mass and draw workgroups decide for themselves)
-    P.ncopy = exact ? pl.nchunk2 + (direct ? 2 : 1) : (direct ? 1 : 0);
+    P.ncopy = decision_copies(exact, pl);
     P.pstride = (int)pl.pstride;
-    const long long unit_bytes = exact ? 2LL * a.gamma * (long long)a.V * (long long)sizeof(typename D::T) : 0;
-    P.y = make_layout(a.B, (long long)P.nslot * pl.nchunk1, pl.nchunk2, direct ? (long long)a.B * pl.nchunkg : 0,
-                      pl.nchunk1, pl.nchunkg, lag_units(a.B, unit_bytes));
-    const long long n_total = (long long)P.y.end2 + (direct ? a.B : 0);
+    P.y = single_pass_layout(a.B, a.gamma, a.V, a.dt, exact, pl);
+    const long long n_total = (long long)P.y.end2 + a.B;
     P.temperature = (double)a.temperature;
     P.alpha = (double)a.alpha;
     P.beta = (double)a.beta;
     P.c = (float)(1.4426950408889634074 / (double)a.temperature);
     P.s = (float)(1.0 / ((double)a.temperature * ((double)a.beta - (double)a.alpha)));
     P.s0 = (float)(-(double)a.alpha / ((double)a.beta - (double)a.alpha));
-    P.error = reinterpret_cast<unsigned int*>(ws) + 1;
+    P.header = reinterpret_cast<unsigned int*>(ws);
     P.dslot = reinterpret_cast<unsigned long long*>(ws + pl.off_dslot);
     P.pslot = reinterpret_cast<unsigned long long*>(ws + pl.off_pslot);
     P.mslot = reinterpret_cast<unsigned long long*>(ws + pl.off_mslot);
@@ -1972,19 +1771,16 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.weight_out = a.weight_out;
     P.mass_out = a.mass_out;
     P.lognorm_out = a.lognorm_out;
-    const long long n_staged = (long long)a.B * (a.gamma * (2LL * pl.nchunk1 + 1) + 1 + pl.nchunkg + pl.nchunk2 + 2);
-    const int gate = gate_stages(a.B, a.V, (long long)sizeof(typename D::T));
-    if (exact && a.staged && direct && a.gammas == nullptr && gate < a.gamma && n_staged <= 0x7fffffffLL) {
+    if (exact && a.staged && a.gammas == nullptr && staged_workgroups(a.B, a.gamma, a.V, a.dt, pl) > 0) {
         // the row-staged early exit (staged_kernel).  The single pass serves
-        // (same results) without the bonus role (small batches with large
-        // vocabularies), past 2^31 workgroups, and when the stream is too
+        // (same results) past 2^31 workgroups and when the stream is too
         // short for any decision row to be gated (gate >= gamma): then the
         // staged order could skip nothing and only lengthens the chain of
         // decisions.
         P.gslot = reinterpret_cast<unsigned long long*>(ws + pl.off_gslot);
         P.gwords = pl.gwords;
         P.gstride = (int)pl.gstride;
-        P.gate = gate;
+        P.gate = gate_stages(a.B, a.V, bytes_per_logit(a.dt));
         P.y = make_staged_layout(a.B, a.gamma, pl.nchunk1, pl.nchunkg, pl.nchunk2);
         const dim3 sgrid((unsigned int)((long long)P.y.end2 + a.B)), sblock(kThreads);
         hipLaunchKernelGGL((staged_kernel<D>), sgrid, sblock, 0, a.stream, P);
@@ -2006,21 +1802,9 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
 }
 
 static sv_status_t run(const Call& a, bool exact) {
-    if (a.draft == nullptr || a.target == nullptr || a.tokens == nullptr || a.uniforms == nullptr ||
-        a.accepted_len == nullptr || a.next_token == nullptr || a.ws == nullptr)
-        return SV_ERR_NULL;
-    if (!valid_dtype(a.dt)) return SV_ERR_DTYPE;
     Plan pl;
-    if (!make_plan(a.B, a.gamma, a.V, a.dt, &pl)) return SV_ERR_SHAPE;
-    if (!(std::isfinite(a.temperature) && a.temperature > 0.0f)) return SV_ERR_PARAM;
-    const double c = 1.4426950408889634074 / (double)a.temperature;
-    if (!(std::isfinite((float)c) && (float)c > 0.0f)) return SV_ERR_PARAM;
-    if (!exact) {
-        if (!(std::isfinite(a.alpha) && std::isfinite(a.beta) && a.alpha < a.beta)) return SV_ERR_PARAM;
-        const double s = 1.0 / ((double)a.temperature * ((double)a.beta - (double)a.alpha));
-        if (!(std::isfinite((float)s) && (float)s > 0.0f)) return SV_ERR_PARAM;
-    }
-    if (a.ws_bytes < pl.bytes || (reinterpret_cast<uintptr_t>(a.ws) & 15u) != 0) return SV_ERR_WORKSPACE;
+    const sv_status_t st = validate(a, exact, &pl);
+    if (st != SV_OK) return st;
     switch (a.dt) {
         case SV_F32: return launch<F32>(a, exact, pl);
         case SV_F16: return launch<F16>(a, exact, pl);
@@ -2049,6 +1833,18 @@ sv_status_t spec_verify_workspace_init(void* workspace, size_t workspace_bytes, 
     const unsigned int blocks = (unsigned int)std::min<size_t>(1024, (n + 255) / 256);
     hipLaunchKernelGGL(sv::fill_zero_kernel, dim3(blocks), dim3(256), 0, stream, static_cast<uint32_t*>(workspace), n);
     return hipGetLastError() == hipSuccess ? SV_OK : SV_ERR_HIP;
+}
+
+sv_status_t spec_verify_workspace_check(const void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (workspace == nullptr) return SV_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0 || workspace_bytes < sv::kHeaderBytes)
+        return SV_ERR_WORKSPACE;
+    uint32_t flag = 0;
+    if (hipMemcpyAsync(&flag, static_cast<const char*>(workspace) + sv::kErrorFlagOffset, sizeof(flag),
+                       hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess)
+        return SV_ERR_HIP;
+    return flag != 0 ? SV_ERR_TIMEOUT : SV_OK;
 }
 
 sv_status_t spec_verify_exact(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
@@ -2139,6 +1935,7 @@ const char* spec_verify_status_string(sv_status_t status) {
         case SV_ERR_WORKSPACE: return "workspace too small or misaligned";
         case SV_ERR_HIP: return "HIP launch failed";
         case SV_ERR_ALLOC: return "host allocation failed";
+        case SV_ERR_TIMEOUT: return "a wait between workgroups timed out; re-initialise the workspace";
     }
     return "unknown status";
 }

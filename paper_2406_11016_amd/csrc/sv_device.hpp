@@ -11,14 +11,9 @@
 #include <math.h>
 #include <stdint.h>
 
-namespace sv {
+#include "plan.hpp"
 
-constexpr int kThreads = 256;            // threads per workgroup (4 wave64s)
-constexpr int kWave = 64;
-constexpr int kWaves = kThreads / kWave;
-constexpr int kMaxGamma = 128;
-constexpr int kMaxRows = 2 * kMaxGamma + 1;
-constexpr int kUnroll = 8;               // 16-byte loads in flight per thread
+namespace sv {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));

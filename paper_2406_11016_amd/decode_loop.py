@@ -12,12 +12,14 @@ token accepted" must hold for all of them.
 The loop owns static device buffers sized for ``gamma_max``.  Whatever
 produces the logits (the draft and target models of a decoder; a synthetic
 source here) writes an iteration's ``[B, gamma, V]`` / ``[B, gamma + 1, V]``
-logits, drafted tokens and uniforms into the leading part of those buffers,
-and the call for each gamma is captured once into a HIP graph (lazily, on
-first use) and replayed, so an iteration costs one graph launch, two small
-device-to-host copies into pinned memory and one stream synchronisation --
-the host needs the accepted length to decide the next gamma and which tokens
-to append.
+logits, drafted tokens and uniforms into the leading part of those buffers;
+an iteration then costs one launch of the step, three small device-to-host
+copies into pinned memory (the accepted lengths, the next tokens and the
+workspace's error flag) and one stream synchronisation -- the host needs the
+accepted length to decide the next gamma and which tokens to append.  With
+``use_graphs`` the call for each gamma is captured once into a HIP graph
+(lazily, on first use) and replayed instead; on ROCm 7 that measured slower
+than launching this one-kernel step directly, so it is off by default.
 """
 from __future__ import annotations
 
@@ -55,7 +57,7 @@ class DecodeLoop:
 
     def __init__(self, batch: int, vocab: int, dtype: str, *, mode: str = "exact", temperature: float = 1.0,
                  alpha: float = -1.0e4, beta: float = 1.0e4, gamma0: int = 5, gamma_max: int = 20,
-                 use_graphs: bool = True, native: bool = False, device="cuda"):
+                 use_graphs: bool = False, native: bool = False, device="cuda"):
         if not (1 <= gamma0 <= gamma_max):
             raise ValueError("need 1 <= gamma0 <= gamma_max")
         self.B, self.V, self.dtype, self.mode = batch, vocab, dtype, mode
@@ -71,6 +73,7 @@ class DecodeLoop:
         self.acc = torch.empty(B, dtype=torch.int32, device=self.device)
         self.nxt = torch.empty(B, dtype=torch.int32, device=self.device)
         self.host = torch.empty(2 * B, dtype=torch.int32, pin_memory=True)
+        self.flag_host = torch.zeros(1, dtype=torch.int32, pin_memory=True)
         ws = max(binding.workspace_bytes(B, g, V, tdt) for g in range(1, G + 1))
         self.ws = torch.zeros((ws + 15) // 16 * 16, dtype=torch.uint8, device=self.device)
         self.stream = torch.cuda.Stream(self.device)
@@ -151,9 +154,20 @@ class DecodeLoop:
         with torch.cuda.stream(self.stream):
             self.host[:B].copy_(self.acc, non_blocking=True)
             self.host[B:].copy_(self.nxt, non_blocking=True)
+            self.flag_host.copy_(self.ws[binding.ERROR_FLAG_OFFSET:binding.ERROR_FLAG_OFFSET + 4].view(torch.int32),
+                                 non_blocking=True)
         self.stream.synchronize()
+        if int(self.flag_host[0]) != 0:
+            raise binding.SpecVerifyError("a wait between workgroups timed out: the outputs are not valid; "
+                                          "re-initialise the workspace (reset_workspace)")
         h = self.host.numpy()
         return h[:B].copy(), h[B:].copy()
+
+    def reset_workspace(self) -> None:
+        """Zero-fill the workspace (after a timed-out wait)."""
+        with torch.cuda.stream(self.stream):
+            binding.init_workspace(self.ws)
+        self.stream.synchronize()
 
     def run(self, producer, iterations: int, stats: Optional[LoopStats] = None,
             time_device: bool = False) -> LoopStats:

@@ -14,6 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "spec_verify.h")
 
 SV_OK, SV_ERR_NULL, SV_ERR_SHAPE, SV_ERR_DTYPE, SV_ERR_PARAM, SV_ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
+SV_ERR_TIMEOUT = -8
 
 
 def declared_functions():
@@ -44,10 +45,25 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_status_strings(lib):
-    for st in (0, -1, -2, -3, -4, -5, -6):
-        assert binding.status_string(st)
+    for st in (0, -1, -2, -3, -4, -5, -6, -7, -8):
+        assert binding.status_string(st) and binding.status_string(st) != "unknown status"
     assert binding.status_string(0) == "ok"
+    assert "timed out" in binding.status_string(SV_ERR_TIMEOUT)
     assert "unknown" in binding.status_string(7)
+
+
+def test_workspace_check_validates_before_touching_the_gpu(lib):
+    f = lib.spec_verify_workspace_check
+    assert f(None, 4096, None) == SV_ERR_NULL
+    assert f(0x7008, 4096, None) == SV_ERR_WORKSPACE    # not 16-byte aligned
+    assert f(0x7000, 255, None) == SV_ERR_WORKSPACE     # smaller than the header
+
+
+def test_out_of_range_dtype_codes_are_rejected(lib):
+    for code in (3, 7, -1, 1 << 30):
+        assert lib.spec_verify_workspace_bytes(2, 3, 100, code) == 0
+        assert _exact(lib, _args(dtype=code)) == SV_ERR_DTYPE
+        assert _sigmoid(lib, _args(dtype=code)) == SV_ERR_DTYPE
 
 
 def test_workspace_bytes(lib):

@@ -104,40 +104,22 @@ def test_gamma_range(gamma, batch, vocab, dtype, noise):
 @pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("V", [1, 2, 7, 65, 300007])
 def test_fall_back_to_the_single_pass(dtype, V):
-    # too short a stream to gate any decision row (and, at the largest
-    # vocabulary, a target row gamma too long for the direct bonus draw):
-    # the single pass runs; the result is the same
+    # too short a stream to gate any decision row (gate >= gamma): the single
+    # pass runs; the result is the same
     x = W.small_case(3, 3, V, dtype, seed=400 + V)
     assert _gate(3, V, dtype) >= 3
     _check(x, f"V={V} {dtype}")
 
 
 @pytest.mark.parametrize("name", ["exact_b1_g5_v51865_f32", "exact_b16_g5_v51865_f32"])
-def test_fall_back_at_small_batch_is_as_fast_as_the_single_pass(name):
+def test_fall_back_on_the_small_batch_workloads(name):
     """The named small-batch workloads gate nothing, so the early exit runs the
-    single pass; its time per call stays within 20% of spec_verify_exact's
-    (the staged kernel took twice as long at B = 1)."""
+    single pass (the host's choice is checked on the CPU by
+    tests/native/plan_check.cpp; the two entry points' times are compared in
+    bench_sweeps.py): the outputs are the single pass's and the oracle's."""
     w = W.WORKLOADS[name]
-    x = W.generate(w)
     assert _gate(w.batch, w.vocab, w.dtype) >= w.gamma
-    d, t, tok, u = binding.to_device(x)
-    ws = binding.new_workspace(w.batch, w.gamma, w.vocab, d.dtype, "cuda")
-
-    def per_call(ee):
-        for _ in range(50):
-            binding.verify(d, t, tok, u, mode="exact", workspace=ws, early_exit=ee)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(500):
-            binding.verify(d, t, tok, u, mode="exact", workspace=ws, early_exit=ee)
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / 500
-
-    single, early = min(per_call(False) for _ in range(3)), min(per_call(True) for _ in range(3))
-    print(f"[early-exit] {name}: single {single * 1e3:.2f} us, early exit {early * 1e3:.2f} us", flush=True)
-    assert early <= 1.2 * single, (single, early)
+    _check(W.generate(w), name)
 
 
 def test_sentinels():

@@ -253,7 +253,7 @@ def test_sigmoid_zero_residual_fallback():
     compare(x, g, o, label="fallback")
 
 
-@pytest.mark.parametrize("idx", range(8))
+@pytest.mark.parametrize("idx", range(9))
 def test_golden_examples_on_gpu(golden_examples, idx):
     ex = golden_examples[idx]
     draft, target, tokens, uniforms = example_arrays(ex, dtype=np.float32)
