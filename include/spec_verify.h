@@ -49,7 +49,9 @@
  * It carries the hand-off between the workgroups of the single launch a call
  * makes.  Calls that share a workspace must be ordered (same stream, or
  * synchronised); concurrent calls need separate workspaces.  There is no
- * mutable global state: the functions are reentrant and thread-safe.
+ * mutable global state other than spec_verify_exact_static's per-device
+ * workspace lookup (guarded by a mutex): the functions are reentrant and
+ * thread-safe.
  *
  * Errors.  Invalid arguments are detected on the host before anything is
  * launched and return a negative status.  Bad data found on the device --
@@ -189,6 +191,35 @@ sv_status_t spec_verify_exact_early_exit(const void* draft_logits, const void* t
                                          int32_t batch, int32_t gamma, int32_t vocab, float temperature,
                                          int32_t* accepted_len, int32_t* next_token,
                                          void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Size of the static device workspace of spec_verify_exact_static, per GPU. */
+#define SV_STATIC_WORKSPACE_BYTES (8u << 20)
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * spec_verify_exact with the library's own static workspace instead of a
+ * caller's.  Same arguments, layout, results and errors as spec_verify_exact,
+ * without workspace / workspace_bytes.
+ *
+ * The workspace is a SV_STATIC_WORKSPACE_BYTES (8 MiB) array in the library's
+ * device code, one per GPU, held until the process ends; nothing is allocated
+ * or freed.  The first call on a device (the current device, which must own
+ * `stream`) looks it up and zero-fills it with a fill kernel on `stream`.
+ * Every call on a GPU shares that GPU's array and leaves it zero-filled, so
+ * calls that overlap in time on one GPU (other streams, other threads) race
+ * and give wrong results: order them.  After a timed-out wait (see
+ * "Timed-out waits") every later call writes the sentinel -1 to every output
+ * until a call passes `reset` nonzero, which zero-fills the array on `stream`
+ * before the step.  Sizes whose spec_verify_workspace_bytes() exceeds
+ * SV_STATIC_WORKSPACE_BYTES (for example B > ~1400 at gamma = 8,
+ * V = 128,256) return SV_ERR_WORKSPACE before anything is launched.
+ */
+sv_status_t spec_verify_exact_static(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                     const int32_t* draft_tokens, const float* uniforms,
+                                     int32_t batch, int32_t gamma, int32_t vocab, float temperature,
+                                     int32_t* accepted_len, int32_t* next_token, int32_t reset,
+                                     hipStream_t stream);
 
 /*
  * Sigmoid mode (Sec. 3.2.2, eq. (5)): p_hat = sigma((z_p / T - alpha) / (beta - alpha))

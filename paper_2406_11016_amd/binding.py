@@ -31,6 +31,7 @@ SYMBOLS = (
     "spec_verify_workspace_check",
     "spec_verify_exact",
     "spec_verify_exact_early_exit",
+    "spec_verify_exact_static",
     "spec_verify_sigmoid",
     "spec_verify_exact_probe",
     "spec_verify_sigmoid_probe",
@@ -92,6 +93,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.spec_verify_exact.restype = ctypes.c_int
     lib.spec_verify_exact_early_exit.argtypes = common + outs
     lib.spec_verify_exact_early_exit.restype = ctypes.c_int
+    lib.spec_verify_exact_static.argtypes = common + [_vp, _vp, _i32, _vp]
+    lib.spec_verify_exact_static.restype = ctypes.c_int
     lib.spec_verify_sigmoid.argtypes = common + [_f32, _f32] + outs
     lib.spec_verify_sigmoid.restype = ctypes.c_int
     lib.spec_verify_exact_probe.argtypes = common + outs + [_vp, _vp, _vp, _vp]
@@ -287,6 +290,27 @@ def verify(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, unif
     if check:
         check_workspace(workspace)
     return (accepted_len, next_token, pr) if probe else (accepted_len, next_token)
+
+
+STATIC_WORKSPACE_BYTES = 8 << 20
+
+
+def verify_static(draft: torch.Tensor, target: torch.Tensor, tokens: torch.Tensor, uniforms: torch.Tensor,
+                  accepted_len: torch.Tensor, next_token: torch.Tensor, *, temperature: float = 1.0,
+                  reset: bool = False) -> None:
+    """spec_verify_exact_static on the current stream: the exact-mode step
+    with the library's static per-GPU workspace (no allocation anywhere; the
+    caller provides the outputs)."""
+    lib = _lib if _lib is not None else load_library()
+    B, g, V = _validate(draft, target, tokens, uniforms)
+    di = draft.get_device()
+    for name, t in (("accepted_len", accepted_len), ("next_token", next_token)):
+        if t.dtype != torch.int32 or tuple(t.shape) != (B,) or not t.is_contiguous() or t.get_device() != di:
+            raise SpecVerifyError(f"{name} must be a contiguous int32 [{B}] tensor on {draft.device}")
+    st = lib.spec_verify_exact_static(_ptr(draft), _ptr(target), DTYPE_CODES[draft.dtype], _ptr(tokens),
+                                      _ptr(uniforms), B, g, V, float(temperature), _ptr(accepted_len),
+                                      _ptr(next_token), 1 if reset else 0, _stream(draft.device))
+    _check(st, "spec_verify_exact_static")
 
 
 def to_device(inputs, device="cuda"):

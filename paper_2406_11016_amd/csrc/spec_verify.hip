@@ -30,6 +30,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "spec_verify.h"
 #include "sv_device.hpp"
@@ -1801,6 +1802,51 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     return hipGetLastError() == hipSuccess ? SV_OK : SV_ERR_HIP;
 }
 
+// ---------------------------------------------------------------------------
+// The static workspace of spec_verify_exact_static (for callers that cannot
+// allocate): one array per GPU in the library's code object, never allocated
+// or freed.  In host code `scratch` only names the symbol; its device address
+// on the current device comes from hipGetSymbolAddress, looked up once per
+// device (which also zero-fills it) and kept until the process ends.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[SV_STATIC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mutex;
+static void* g_scratch_ptr[kMaxDevices] = {};
+
+static void launch_fill(void* p, size_t bytes, hipStream_t stream) {
+    const size_t n = bytes / 4;
+    const unsigned int blocks = (unsigned int)std::min<size_t>(1024, (n + 255) / 256);
+    hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, stream, static_cast<uint32_t*>(p), n);
+}
+
+// The current device's static workspace (zero-filled on `stream` the first
+// time a device asks), or nullptr with *st set on a HIP error.
+static void* static_workspace(hipStream_t stream, sv_status_t* st) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        *st = SV_ERR_HIP;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) {
+            *st = SV_ERR_HIP;
+            return nullptr;
+        }
+        launch_fill(ptr, SV_STATIC_WORKSPACE_BYTES, stream);
+        if (hipGetLastError() != hipSuccess) {
+            *st = SV_ERR_HIP;
+            return nullptr;
+        }
+        g_scratch_ptr[dev] = ptr;
+    }
+    *st = SV_OK;
+    return g_scratch_ptr[dev];
+}
+
 static sv_status_t run(const Call& a, bool exact) {
     Plan pl;
     const sv_status_t st = validate(a, exact, &pl);
@@ -1854,6 +1900,28 @@ sv_status_t spec_verify_exact(const void* draft_logits, const void* target_logit
     sv::Call a{draft_logits, target_logits, dtype, draft_tokens, uniforms, batch, gamma, vocab, temperature,
                0.0f, 0.0f, accepted_len, next_token, workspace, workspace_bytes, stream,
                nullptr, nullptr, nullptr, nullptr, nullptr};
+    return sv::run(a, true);
+}
+
+sv_status_t spec_verify_exact_static(const void* draft_logits, const void* target_logits, sv_dtype_t dtype,
+                                     const int32_t* draft_tokens, const float* uniforms, int32_t batch,
+                                     int32_t gamma, int32_t vocab, float temperature, int32_t* accepted_len,
+                                     int32_t* next_token, int32_t reset, hipStream_t stream) {
+    // the arguments first, against a stand-in workspace of the static size
+    // (only its size and alignment are checked)
+    sv::Call a{draft_logits, target_logits, dtype, draft_tokens, uniforms, batch, gamma, vocab, temperature,
+               0.0f, 0.0f, accepted_len, next_token, reinterpret_cast<void*>(uintptr_t{256}),
+               SV_STATIC_WORKSPACE_BYTES, stream, nullptr, nullptr, nullptr, nullptr, nullptr};
+    sv::Plan pl;
+    const sv_status_t valid = sv::validate(a, true, &pl);
+    if (valid != SV_OK) return valid;
+    sv_status_t st = SV_OK;
+    a.ws = sv::static_workspace(stream, &st);
+    if (a.ws == nullptr) return st;
+    if (reset != 0) {
+        sv::launch_fill(a.ws, pl.bytes, stream);
+        if (hipGetLastError() != hipSuccess) return SV_ERR_HIP;
+    }
     return sv::run(a, true);
 }
 
