@@ -245,6 +245,44 @@ def unfused_baseline(w, sets, tok, uni, steps: int, warmup: int):
                                     "eq. (1), cumprod scan, residual, cumsum + searchsorted (fp32)"}
 
 
+def divergence_from_exact(w, dev, input_sets: int = 4) -> dict:
+    """How far the sigmoid approximation's decisions are from the exact mode's
+    on the same inputs (Sec. 3.2.2; the workload's own comparison): both modes
+    run through the GPU path with their probe outputs on ``input_sets`` seeded
+    input sets of the workload's shape.  Acceptance rate = mean accepted
+    length / gamma; TV = half the L1 distance between the two modes' final
+    distributions (the weights divided by their mass) of each element; token
+    disagreement = fraction of elements whose next tokens differ."""
+    import numpy as np
+    import torch
+
+    from paper_2406_11016_amd import binding
+    from paper_2406_11016_amd import workloads as W
+    acc_s, acc_e, tv, dis = [], [], [], []
+    for k in range(input_sets):
+        x = W.generate(w, seed=w.seed * 100 + k)
+        d, t, tok, u = binding.to_device(x, dev)
+        res = {}
+        for mode in ("sigmoid", "exact"):
+            a, n, pr = binding.verify(d, t, tok, u, mode=mode, temperature=w.temperature, alpha=w.alpha,
+                                      beta=w.beta, probe=True)
+            res[mode] = (a, n, pr.weights.double() / pr.mass[:, None])
+        (a_s, n_s, f_s), (a_e, n_e, f_e) = res["sigmoid"], res["exact"]
+        ok = (a_s >= 0) & (a_e >= 0)
+        acc_s.append(a_s[ok].double().cpu().numpy() / w.gamma)
+        acc_e.append(a_e[ok].double().cpu().numpy() / w.gamma)
+        tv.append((0.5 * (f_s[ok] - f_e[ok]).abs().sum(-1)).cpu().numpy())
+        dis.append((n_s[ok] != n_e[ok]).double().cpu().numpy())
+    torch.cuda.synchronize()
+    acc_s, acc_e, tv, dis = (np.concatenate(v) for v in (acc_s, acc_e, tv, dis))
+    return {"elements": int(acc_s.size), "accept_rate_sigmoid": round(float(acc_s.mean()), 4),
+            "accept_rate_exact": round(float(acc_e.mean()), 4),
+            "accept_rate_delta": round(float(acc_s.mean() - acc_e.mean()), 4),
+            "mean_tv_final": round(float(tv.mean()), 4), "token_disagreement": round(float(dis.mean()), 4),
+            "what": f"GPU path, both modes with probes on {input_sets} seeded input sets of this shape; "
+                    "acceptance = mean accepted length / gamma, TV between the two modes' final distributions"}
+
+
 def copy_calibration(nbytes: int, reps: int) -> None:
     """A plain device-to-device copy of known size, for scaling HBM counters."""
     import torch
@@ -376,6 +414,11 @@ def main() -> int:
                 "kernel": "verify_kernel<exact> (the whole step is one launch)" if w.mode == "exact"
                 else "verify_kernel<sigmoid> (the whole step is one launch)", "algorithmic_bytes_per_step": alg}
 
+    divergence = None
+    if w.mode == "sigmoid":
+        log("divergence from the exact mode on the same inputs")
+        divergence = divergence_from_exact(w, dev)
+
     unfused = None
     if not args.no_unfused:
         log("timing the unfused PyTorch comparison")
@@ -395,6 +438,8 @@ def main() -> int:
         "cpu_baseline": cpu,
         "unfused_torch": unfused,
     }
+    if divergence is not None:
+        out["divergence_from_exact"] = divergence
     print(json.dumps(out), flush=True)
     return 0
 

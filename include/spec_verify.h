@@ -36,8 +36,8 @@
  *   uniforms       [B, gamma+1]     fp32 in [0, 1)
  *   accepted_len   [B]              int32 out, L in [0, gamma]
  *   next_token     [B]              int32 out, in [0, V)
- * Rows need no particular alignment; 16-byte aligned rows are read with
- * 128-bit loads.
+ * Rows need no particular alignment; rows starting at a 4-byte aligned
+ * address (every fp32 row, 16-bit rows of even V) are read with 128-bit loads.
  *
  * Ownership and concurrency.  Every pointer is owned by the caller.  The
  * library never allocates device memory and never prints; only

@@ -126,7 +126,7 @@ struct SigmoidWeights {
 template <class D>
 __device__ __forceinline__ bool pair_aligned(const typename D::T* rp, const typename D::T* rq, bool two_rows) {
     const uintptr_t a = reinterpret_cast<uintptr_t>(rp) | (two_rows ? reinterpret_cast<uintptr_t>(rq) : 0);
-    return (a & 15u) == 0;
+    return (a & 3u) == 0;
 }
 
 // Vectors v0 + u * vstride (u < U) from a chunk of n elements of the selected
@@ -596,8 +596,8 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot,
     const Span sp = sub_chunk(k, wave, chunk, V, E);
     const T* base = row + sp.begin;
     const int n = sp.n;
-    const int nfull = n / E;  // whole 16-byte vectors
-    const bool aligned = (reinterpret_cast<uintptr_t>(base) & 15u) == 0;
+    const int nfull = n / E;  // whole vectors of E elements
+    const bool aligned = vec_loadable(base);
 
     // Lane l takes whole vectors l, l + 64, ... of the quarter in blocks of
     // kUnroll; all loads of a block are issued before any is used, and the
@@ -615,7 +615,7 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot,
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) unpack<D>(raw[u], x[u]);
         } else {
-            // rows that are not 16-byte aligned (e.g. odd V in fp32)
+            // rows that are not 4-byte aligned (16-bit logits with odd V)
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u)
                 load_elems_or_pad<D>(base, (v0 + u * kWave + lane) * E, nfull * E, x[u]);
@@ -1078,7 +1078,7 @@ __device__ __forceinline__ int wave_find_target(const typename D::T* rp, int n, 
     constexpr int NV = 4;
     constexpr int NE = NV * E;
     const int lane = threadIdx.x % kWave;
-    const bool fast = (reinterpret_cast<uintptr_t>(rp) & 15u) == 0;
+    const bool fast = vec_loadable(rp);
     float z[NV][E], zq[NV][E];
     load_pair_u<D, NV>(rp, rp, false, fast, lane * NV, 1, n, z, zq);
     // the weights are recomputed where needed rather than kept (registers)

@@ -16,6 +16,10 @@
 namespace sv {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+// 16 bytes at a 4-byte aligned address: still one global_load_dwordx4, so
+// rows whose start is only 4-byte aligned (fp32 rows of odd length, 16-bit
+// rows of even length) stream as fast as 16-byte aligned ones
+typedef unsigned int u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 // ---------------------------------------------------------------------------
@@ -69,10 +73,8 @@ __device__ __forceinline__ void unpack<F16>(const u32x4 r, float (&x)[8]) {
     for (int e = 0; e < 8; ++e) x[e] = (float)h[e];
 }
 
-template <class D>
-__device__ __forceinline__ u32x4 load16(const typename D::T* p) {
-    return *reinterpret_cast<const u32x4*>(p);
-}
+// Whether 16-byte vector loads may start at p (any 4-byte aligned address).
+__device__ __forceinline__ bool vec_loadable(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 // A 16-byte vector whose every element is -inf in storage type D.
 template <class D>
@@ -84,12 +86,15 @@ __device__ __forceinline__ u32x4 neg_inf_vec<F16>() { return u32x4{0xfc00fc00u, 
 template <>
 __device__ __forceinline__ u32x4 neg_inf_vec<BF16>() { return u32x4{0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u}; }
 
-// Vector v of a 16-byte aligned chunk holding nfull (>= 1) whole vectors, or
-// the -inf vector when v >= nfull.  The load is unconditional (its index is
-// clamped into range) so that a block of such loads is issued back to back.
+// Vector v (elements v E .. v E + E - 1) of a chunk starting at a 4-byte
+// aligned address and holding nfull (>= 1) whole vectors, or the -inf vector
+// when v >= nfull.  The load is unconditional (its index is clamped into
+// range) so that a block of such loads is issued back to back.  The element
+// assignment does not depend on the chunk's address, so equal rows give
+// equal bits wherever they are.
 template <class D, bool NT>
 __device__ __forceinline__ u32x4 load_vec_or_pad(const typename D::T* base, int v, int nfull) {
-    const u32x4* p = reinterpret_cast<const u32x4*>(base + (size_t)min(v, nfull - 1) * D::E);
+    const u32x4_a4* p = reinterpret_cast<const u32x4_a4*>(base + (size_t)min(v, nfull - 1) * D::E);
     const u32x4 r = NT ? __builtin_nontemporal_load(p) : *p;
     return (v < nfull) ? r : neg_inf_vec<D>();
 }

@@ -7,6 +7,8 @@ probabilities must match within 1e-5 relative (fp32 logits) or 2e-3
 import math
 
 import numpy as np
+import scipy.special
+import scipy.stats
 import pytest
 import torch
 
@@ -319,6 +321,46 @@ def test_gpu_emits_target_distribution_tiny_vocab():
         counts = np.bincount(emitted, minlength=V)
         sigma = np.sqrt(m * P[c] * (1 - P[c]))
         assert np.all(np.abs(counts - m * P[c]) <= 3 * sigma), (c, counts, m * P[c], sigma)
+
+
+@pytest.mark.parametrize("alpha,beta,seed", [(-10.0, 10.0, 31), (-3.0, 3.0, 32)])
+def test_gpu_sigmoid_first_token_law_tiny_vocab(alpha, beta, seed):
+    """10^6 seeded steps of the sigmoid mode through the GPU with fixed rows
+    and drafts x ~ q (the draft's softmax): the first emitted token has the
+    law q tau_hat + (1 - sum q tau_hat) a_hat / b_hat of the approximate test
+    and residual of Sec. 3.2.2 (the same closed form as the oracle's CPU
+    check), within a Bonferroni bar of 1e-4 family-wise.  Seeds fixed in
+    advance."""
+    gamma, V, n, T = 2, 6, 1_000_000, 1.0
+    g = np.random.Generator(np.random.PCG64(seed))
+    z_p = g.normal(0, 8, size=(gamma + 1, V)).astype(np.float32)
+    z_q = (z_p[:gamma] + g.normal(0, 8, size=(gamma, V))).astype(np.float32)
+    tokens = np.stack([W.gumbel_max_tokens(g, np.broadcast_to(z_q[c].astype(np.float64), (n, V)), T)
+                       for c in range(gamma)], axis=1)
+    u = np.minimum(g.random((n, gamma + 1)).astype(np.float32), W.UNIFORM_MAX)
+    x = W.Inputs(np.ascontiguousarray(np.broadcast_to(z_q, (n, gamma, V))),
+                 np.ascontiguousarray(np.broadcast_to(z_p, (n, gamma + 1, V))), tokens, u, "f32", "sigmoid", T,
+                 alpha, beta)
+    acc, nxt = run_gpu(x, probe=False)
+    assert np.all(acc >= 0)
+    first = np.where(acc >= 1, tokens[:, 0], nxt)
+    zp0, zq0 = z_p[0].astype(np.float64), z_q[0].astype(np.float64)
+    ph = scipy.special.expit((zp0 / T - alpha) / (beta - alpha))
+    qh = scipy.special.expit((zq0 / T - alpha) / (beta - alpha))
+    q = scipy.special.softmax(zq0 / T)
+    tau = np.minimum(1.0, ph / qh)
+    resid = np.maximum(0.0, ph - qh)
+    law = q * tau + (1.0 - np.sum(q * tau)) * resid / resid.sum()
+    assert abs(law.sum() - 1.0) < 1e-12
+    k = int(np.sum(law > 0))
+    nsigma = float(scipy.stats.norm.isf(1e-4 / (2 * k)))
+    counts = np.bincount(first, minlength=V)
+    sigma = np.sqrt(n * law * (1 - law))
+    dev = np.abs(counts - n * law)
+    print(f"[sigmoid law] alpha={alpha}: max deviation {np.max(dev / np.maximum(sigma, 1e-12)):.2f} sigma "
+          f"(bar {nsigma:.2f})", flush=True)
+    assert np.all(dev <= nsigma * sigma + 1e-9), (counts, n * law, sigma)
+    assert np.all(counts[law == 0] == 0)
 
 
 # --- seeded random shapes ------------------------------------------------------
