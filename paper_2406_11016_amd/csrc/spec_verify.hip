@@ -697,6 +697,29 @@ __device__ __forceinline__ void sigmoid_row_role(const StepParams& P, int b, int
     }
 }
 
+// log2(s) for a finite s > 0, to about 1.3e-7 absolute: s = M 2^e exactly
+// (M in [1, 2)), log2(M) from the hardware fp32 logarithm of M rounded to
+// fp32 (within an ulp of log2(M) < 1, i.e. 1.2e-7) plus the first-order term
+// of the rounding, (M - m) / (m ln 2).  The decision margin the parity bar
+// allows is 1e-6, and the one-pass fp64 chain this replaces was a long
+// dependent path on the step's critical chain.
+__device__ __forceinline__ double log2_pos(double s) {
+    int e;
+    const double M = 2.0 * frexp(s, &e);  // [1, 2)
+    const float m = (float)M;
+    return (double)(e - 1) + (double)__builtin_amdgcn_logf(m) + (M - (double)m) / ((double)m * 0.6931471805599453094);
+}
+
+// 2^l for l <= 0 (larger l return 1, the clamp of eq. (1)), to about 1.5e-7
+// relative: 2^floor(l) exactly times the hardware fp32 2^f of the fraction
+// f = l - floor(l) in [0, 1) (its fp32 rounding adds under 3e-8).
+__device__ __forceinline__ double exp2_nonpos(double l) {
+    if (!(l < 0.0)) return (l == l) ? 1.0 : l;
+    if (l < -1074.0) return 0.0;
+    const double fl = floor(l);
+    return ldexp((double)__builtin_amdgcn_exp2f((float)(l - fl)), (int)fl);
+}
+
 // Row log2-normalisers Lambda = Kmax + log2(sum S 2^(K - Kmax)) of R rows
 // from the (K, S) pairs of their W sub-chunks in LDS, into sm.rowL: row i
 // belongs to an aligned group of G lanes (the largest power of two <= 16 with
@@ -725,7 +748,8 @@ __device__ __forceinline__ void merge_rows(Smem& sm, int R, int W, int Rg = 0) {
         sum = group_sum(sum, G);
         // a NaN logit makes S NaN; a +inf logit makes K +inf and S NaN
         if (row && g == 0)
-            sm.rowL[i] = (sum != sum) ? __builtin_nan("") : ((m == -INFINITY) ? -INFINITY : (double)m + log2(sum));
+            sm.rowL[i] = (sum != sum) ? __builtin_nan("")
+                         : ((m == -INFINITY) ? -INFINITY : (double)m + ((sum > 0.0 && sum < INFINITY) ? log2_pos(sum) : log2(sum)));
     }
     __syncthreads();
 }
@@ -837,7 +861,7 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
                 tau = 1.0;  // q(x) = 0
             } else {
                 const double l2 = ((double)zp - (double)zq) * (double)P.c - (lam_p - lam_q);
-                tau = min1(exp2(l2));
+                tau = exp2_nonpos(l2);
             }
         } else {
             const double span = P.beta - P.alpha;
@@ -1579,7 +1603,7 @@ __device__ __forceinline__ void row_decider_role(const StepParams& P, int b, int
         const double lam_p = sm.rowL[0], lam_q = sm.rowL[1];
         const bool row_ok = isfinite(lam_p) && isfinite(lam_q);
         double tau = 1.0;  // q(x) = 0
-        if (zq != -INFINITY) tau = min1(exp2(((double)zp - (double)zq) * (double)P.c - (lam_p - lam_q)));
+        if (zq != -INFINITY) tau = exp2_nonpos(((double)zp - (double)zq) * (double)P.c - (lam_p - lam_q));
         sm.result = !row_ok ? 2 : ((r <= tau) ? 0 : 1);
     }
     const bool tok_bad = __syncthreads_or(!tok_ok) != 0;
