@@ -261,6 +261,15 @@ inline Layout single_pass_layout(long long B, long long gamma, long long V, sv_d
                        lag_units(B, unit_bytes));
 }
 
+// Whether the single pass (exact mode, not ragged) waits with two polls in
+// flight: where the decision rows' stream is shorter than the mass lag, the
+// step after the stream is a chain of waits (decision, masses, draw) that
+// the quicker detection shortens.  On long streams the second poll measured
+// slower, so they keep one.
+inline bool pipelined_waits(long long B, long long gamma, long long V, sv_dtype_t dt) {
+    return 2LL * gamma * V * bytes_per_logit(dt) * B < kLagStreamBytes;
+}
+
 // Copies of each decision record, one per reader: every mass workgroup, the
 // draw and the bonus workgroup (exact mode); only the bonus workgroup
 // (sigmoid mode, whose mass and draw workgroups decide for themselves).

@@ -212,57 +212,115 @@ __device__ __forceinline__ unsigned long long pack2(float a, float b) {
 __device__ __forceinline__ float unpack_hi(unsigned long long w) { return __uint_as_float((unsigned int)(w >> 32)); }
 __device__ __forceinline__ float unpack_lo(unsigned long long w) { return __uint_as_float((unsigned int)w); }
 
+// A workgroup barrier for LDS data only: it waits for the workgroup's LDS
+// (and scalar) accesses but not for its global loads and stores in flight,
+// which __syncthreads would.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Sleep between the two polls in flight of a wait (s_sleep units of 64
+// clocks: about 0.05 us; a shorter gap measured faster).
+constexpr int kPollGap = 2;
+
 // Waits until the n words at p are published, handing each to take(i, w)
 // (w the raw, still inverted word).  Called by every thread; returns false
 // after `limit` polls.  Each poll issues NV loads per thread before it
 // looks at any (indices clamped into range), so a poll costs one memory
-// round trip for up to NV * kThreads words.
-template <int NV, class A, class F>
+// round trip for up to NV * kThreads words.  With kPipe (the launch of short
+// streams, whose steps are a chain of such waits) and up to NV * kThreads
+// words, two polls are in flight at once, the second issued a fraction of a
+// round trip after the first, so a word is seen sooner after it lands; the
+// workgroup then agrees on "all present" through LDS flags (a
+// __syncthreads_or would also wait for the other poll's loads).
+template <int NV, bool kPipe = false, class A, class F>
 __device__ __forceinline__ bool poll_at(int n, A addr, F take, int limit) {
-    for (int spin = 0;; ++spin) {
-        int missing = 0;
-        for (int i0 = 0; i0 < n; i0 += NV * kThreads) {
-            unsigned long long w[NV];
+    if (!kPipe || n > NV * kThreads) {
+        for (int spin = 0;; ++spin) {
+            int missing = 0;
+            for (int i0 = 0; i0 < n; i0 += NV * kThreads) {
+                unsigned long long w[NV];
 #pragma unroll
-            for (int u = 0; u < NV; ++u) {
-                const int i = min(i0 + u * kThreads + (int)threadIdx.x, n - 1);
-                w[u] = __hip_atomic_load(addr(i), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
+                for (int u = 0; u < NV; ++u) {
+                    const int i = min(i0 + u * kThreads + (int)threadIdx.x, n - 1);
+                    w[u] = __hip_atomic_load(addr(i), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
 #pragma unroll
-            for (int u = 0; u < NV; ++u) {
-                const int i = i0 + u * kThreads + (int)threadIdx.x;
-                if (i < n) {
-                    if (w[u] == 0ull)
-                        missing = 1;
-                    else
-                        take(i, w[u]);
+                for (int u = 0; u < NV; ++u) {
+                    const int i = i0 + u * kThreads + (int)threadIdx.x;
+                    if (i < n) {
+                        if (w[u] == 0ull)
+                            missing = 1;
+                        else
+                            take(i, w[u]);
+                    }
                 }
             }
+            if (__syncthreads_or(missing) == 0) return true;
+            if (spin >= limit) return false;
+            __builtin_amdgcn_s_sleep(2);
         }
-        if (__syncthreads_or(missing) == 0) return true;
-        if (spin >= limit) return false;
-        __builtin_amdgcn_s_sleep(2);
+    }
+    __shared__ int pflag[2][kWaves];  // "a word is missing", per wave, for two rounds
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    unsigned long long a[NV], c[NV];
+    auto issue = [&](unsigned long long (&w)[NV]) {
+#pragma unroll
+        for (int u = 0; u < NV; ++u)
+            w[u] = __hip_atomic_load(addr(min(u * kThreads + tid, n - 1)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
+    auto check = [&](unsigned long long (&w)[NV], int round) {
+        bool missing = false;
+#pragma unroll
+        for (int u = 0; u < NV; ++u) {
+            const int i = u * kThreads + tid;
+            if (i < n) {
+                if (w[u] == 0ull)
+                    missing = true;
+                else
+                    take(i, w[u]);
+            }
+        }
+        const unsigned long long m = __ballot(missing);
+        if (lane == 0) pflag[round & 1][wave] = (m != 0ull) ? 1 : 0;
+        lds_barrier();
+        int any = 0;
+#pragma unroll
+        for (int w2 = 0; w2 < kWaves; ++w2) any |= pflag[round & 1][w2];
+        return any == 0;
+    };
+    issue(a);
+    for (int round = 0;; round += 2) {
+        __builtin_amdgcn_s_sleep(kPollGap);
+        issue(c);
+        if (check(a, round)) return true;
+        if (round + 1 >= limit) return false;
+        __builtin_amdgcn_s_sleep(kPollGap);
+        issue(a);
+        if (check(c, round + 1)) return true;
+        if (round + 2 >= limit) return false;
     }
 }
 
-template <int NV, class F>
+template <int NV, bool kPipe = false, class F>
 __device__ __forceinline__ bool poll_words(unsigned long long* p, int n, F take, int limit) {
-    return poll_at<NV>(n, [&](int i) { return p + i; }, take, limit);
+    return poll_at<NV, kPipe>(n, [&](int i) { return p + i; }, take, limit);
 }
 
 // The n (<= kThreads) raw record words at p, copied to dst.
+template <bool kPipe = false>
 __device__ __forceinline__ bool wait_raw(unsigned long long* p, int n, unsigned long long* dst, int limit) {
-    return poll_words<1>(p, n, [&](int i, unsigned long long w) { dst[i] = ~w; }, limit);
+    return poll_words<1, kPipe>(p, n, [&](int i, unsigned long long w) { dst[i] = ~w; }, limit);
 }
 
 // The n words at p, decoded to dst (LDS).
+template <bool kPipe = false>
 __device__ __forceinline__ bool wait_words(unsigned long long* p, int n, double* dst, int limit) {
-    return poll_words<4>(p, n, [&](int i, unsigned long long w) { dst[i] = decode_word(w); }, limit);
+    return poll_words<4, kPipe>(p, n, [&](int i, unsigned long long w) { dst[i] = decode_word(w); }, limit);
 }
 
 // The n (K, S) word pairs at p, decoded to K[i] (float) and S[i] (LDS).
+template <bool kPipe = false>
 __device__ __forceinline__ bool wait_ks(unsigned long long* p, int n, float* K, double* S, int limit) {
-    return poll_words<4>(p, 2 * n, [&](int i, unsigned long long w) {
+    return poll_words<4, kPipe>(p, 2 * n, [&](int i, unsigned long long w) {
         if (i & 1)
             S[i >> 1] = decode_word(w);
         else
@@ -815,7 +873,7 @@ struct Decision {
 
 // The decision for batch element b: eq. (1) at the drafted tokens and the
 // first-rejection scan, plus the weights of the final distribution.
-template <class D, bool kExact, bool kRagged>
+template <class D, bool kExact, bool kRagged, bool kPipe = false>
 __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
     const int gamma = P.gamma, V = P.V;
@@ -845,7 +903,7 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
         // the stats slots the decision reads, merged into log2-normalisers
         // max K + log2(sum S 2^(K - max K)) by exact power-of-two scaling
         const int W = P.nchunk1;  // chunks per row
-        d.ok = wait_ks(P.pslot + (size_t)b * P.pstride, 2 * gamma * W, sm.K, sm.S, spin_limit(P));
+        d.ok = wait_ks<kPipe>(P.pslot + (size_t)b * P.pstride, 2 * gamma * W, sm.K, sm.S, spin_limit(P));
         merge_rows(sm, 2 * gamma, W);
     }
 
@@ -1032,11 +1090,11 @@ __device__ __forceinline__ void publish_decision(const StepParams& P, int b, con
     }
 }
 
-template <class D, bool kExact, bool kRagged>
+template <class D, bool kExact, bool kRagged, bool kPipe = false>
 __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& sm) {
     const int gamma = P.gamma, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
-    const Decision d = decide<D, kExact, kRagged>(P, b, sm);
+    const Decision d = decide<D, kExact, kRagged, kPipe>(P, b, sm);
     if (!d.ok && tid == 0) set_error(P);
     // (sigmoid mode: the mass and draw workgroups decide for themselves, so
     // the only copy, if any, is the bonus workgroup's)
@@ -1053,10 +1111,11 @@ __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& s
 
 // Copy `copy` of b's published decision (in b's mass, draw and bonus
 // workgroups), cleared once read.
+template <bool kPipe = false>
 __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, int copy, bool exact, Smem& sm) {
     Decision d{};
     unsigned long long* src = P.dslot + ((size_t)b * P.ncopy + copy) * kDecisionWords;
-    d.ok = wait_raw(src, kDecisionWords, sm.rec, spin_limit(P));
+    d.ok = wait_raw<kPipe>(src, kDecisionWords, sm.rec, spin_limit(P));
     if ((int)threadIdx.x < kDecisionWords) clear_word(src + threadIdx.x);
     const unsigned long long w0 = sm.rec[0];
     d.L = d.ok ? (int)(w0 & 0xffff) : 0;
@@ -1173,7 +1232,7 @@ __device__ __forceinline__ void bonus_probes(const StepParams& P, int b, int gb,
 // quarters (see bonus_role): the same steps as the workgroup version, with
 // every value in registers and no workgroup barrier, since this chain ends
 // the step.  The other waves of the workgroup return at once.
-template <class D, bool kExact, bool kRagged>
+template <class D, bool kExact, bool kRagged, bool kPipe = false>
 __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
     using T = typename D::T;
     if (threadIdx.x >= kWave) return;
@@ -1191,15 +1250,44 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
     const int q = min(lane, W - 1);
     unsigned long long wk = 0ull, ws = 0ull;
     bool ok = false;
-    for (int spin = 0;; ++spin) {
-        wk = __hip_atomic_load(words + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        ws = __hip_atomic_load(words + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (__ballot(lane < W && (wk == 0ull || ws == 0ull)) == 0ull) {
-            ok = true;
-            break;
+    if constexpr (!kPipe) {
+        for (int spin = 0;; ++spin) {
+            wk = __hip_atomic_load(words + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            ws = __hip_atomic_load(words + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (__ballot(lane < W && (wk == 0ull || ws == 0ull)) == 0ull) {
+                ok = true;
+                break;
+            }
+            if (spin >= limit) break;
+            __builtin_amdgcn_s_sleep(2);
         }
-        if (spin >= limit) break;
-        __builtin_amdgcn_s_sleep(2);
+    } else {
+        // two polls in flight, as in poll_at
+        unsigned long long ka, sa, kb, sb;
+        ka = __hip_atomic_load(words + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sa = __hip_atomic_load(words + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int spin = 0;; spin += 2) {
+            __builtin_amdgcn_s_sleep(kPollGap);
+            kb = __hip_atomic_load(words + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            sb = __hip_atomic_load(words + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (__ballot(lane < W && (ka == 0ull || sa == 0ull)) == 0ull) {
+                wk = ka;
+                ws = sa;
+                ok = true;
+                break;
+            }
+            if (spin + 1 >= limit) break;
+            __builtin_amdgcn_s_sleep(kPollGap);
+            ka = __hip_atomic_load(words + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            sa = __hip_atomic_load(words + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (__ballot(lane < W && (kb == 0ull || sb == 0ull)) == 0ull) {
+                wk = kb;
+                ws = sb;
+                ok = true;
+                break;
+            }
+            if (spin + 2 >= limit) break;
+        }
     }
     // the decision copy, in flight during the draw
     unsigned long long rw = 0ull;
@@ -1267,14 +1355,14 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
 // With at most kWave quarters one wave does all of it (bonus_wave_role);
 // otherwise the workgroup, one vector per thread.  It is the only reader of
 // row gamma's words and of its decision copy, and clears them.
-template <class D, bool kExact, bool kRagged>
+template <class D, bool kExact, bool kRagged, bool kPipe = false>
 __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
     const int gamma = P.gamma, V = P.V, R = 2 * gamma + 1;
     const int tid = threadIdx.x;
     const int W = kWaves * P.nchunkg;  // quarters of the row's tiles
     if (W <= kWave) {
-        bonus_wave_role<D, kExact, kRagged>(P, b);
+        bonus_wave_role<D, kExact, kRagged, kPipe>(P, b);
         return;
     }
     bool gbad;
@@ -1288,7 +1376,7 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
     // so it runs while b's decider may still be at work (the last elements'
     // decisions publish after the stream has ended), and the decision is read
     // only before the outputs are written
-    const bool ok = poll_at<4>(2 * W, [&](int i) { return words + i; }, [&](int i, unsigned long long w) {
+    const bool ok = poll_at<4, kPipe>(2 * W, [&](int i) { return words + i; }, [&](int i, unsigned long long w) {
         if (i & 1)
             sm.S[i >> 1] = decode_word(w);
         else
@@ -1340,7 +1428,7 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
         if (tid < kDecisionWords) sm.rec[tid] = ~rw;
         __syncthreads();
     } else {
-        rok = wait_raw(rec, kDecisionWords, sm.rec, limit);
+        rok = wait_raw<kPipe>(rec, kDecisionWords, sm.rec, limit);
     }
     if (tid < kDecisionWords) clear_word(rec + tid);
     if (!(ok && rok) && tid == 0) set_error(P);
@@ -1360,19 +1448,19 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
 // itself (eq. (5) at the 2 gamma drafted-token logits needs no row
 // normaliser, and the decision code is deterministic, so every workgroup of b
 // reaches the same one), which spares the hand-off from the decider.
-template <class D, bool kExact, bool kRagged>
+template <class D, bool kExact, bool kRagged, bool kPipe = false>
 __device__ __forceinline__ Decision decision_of(const StepParams& P, int b, int copy, Smem& sm) {
-    if constexpr (kExact) return read_decision(P, b, copy, true, sm);
+    if constexpr (kExact) return read_decision<kPipe>(P, b, copy, true, sm);
     return decide<D, false, kRagged>(P, b, sm);
 }
 
-template <class D, bool kExact, bool kRagged>
+template <class D, bool kExact, bool kRagged, bool kPipe = false>
 __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Smem& sm) {
     using T = typename D::T;
     constexpr int E = D::E;
     const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-    const Decision d = decision_of<D, kExact, kRagged>(P, b, k2, sm);
+    const Decision d = decision_of<D, kExact, kRagged, kPipe>(P, b, k2, sm);
     if (!d.ok && tid == 0) set_error(P);
     // b's bonus workgroup draws when every draft is accepted: nothing to do here
     const bool drawn = !d.bad && d.L == d.gb;
@@ -1393,7 +1481,7 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
 // The inverse-CDF draw for b, by b's draw workgroup, once b's mass tiles have
 // published (unless b's bonus workgroup draws); then clears b's mass words
 // for the next call.
-template <class D, bool kExact, bool kRagged>
+template <class D, bool kExact, bool kRagged, bool kPipe = false>
 __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) {
     using T = typename D::T;
     constexpr int E = D::E;
@@ -1401,13 +1489,13 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int M = P.nchunk2 * kWaves;
     const bool sticky = sticky_error(P);
-    Decision d = decision_of<D, kExact, kRagged>(P, b, P.nchunk2, sm);
+    Decision d = decision_of<D, kExact, kRagged, kPipe>(P, b, P.nchunk2, sm);
     // b's bonus workgroup writes the outputs when every draft is accepted
     const bool drawn = !d.bad && d.L == d.gb;
     if (!d.ok && tid == 0) set_error(P);
     if (drawn) return;
     unsigned long long* ms = P.mslot + (size_t)b * M;
-    const bool got = d.ok && wait_words(ms, M, sm.sub, spin_limit(P));
+    const bool got = d.ok && wait_words<kPipe>(ms, M, sm.sub, spin_limit(P));
     if (d.ok && !got && tid == 0) set_error(P);
     const double u = (double)P.uniforms[(size_t)b * (gamma + 1) + d.gb];
     const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V;
@@ -1647,7 +1735,7 @@ __device__ __forceinline__ void row_decider_role(const StepParams& P, int b, int
     }
 }
 
-template <class D, bool kExact, bool kRagged>
+template <class D, bool kExact, bool kRagged, bool kPipe = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void verify_kernel(StepParams P) {
     __shared__ Smem sm;
     // one argument fetch for the role split and the stats role (see Layout)
@@ -1686,7 +1774,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         r = loc - k * Y.size2 + (unsigned int)Y.S + 1u;
         bm = Y.b2 + (int)k;
     } else {
-        bonus_role<D, kExact, kRagged>(P, (int)(id - Y.end2), sm);
+        bonus_role<D, kExact, kRagged, kPipe>(P, (int)(id - Y.end2), sm);
         return;
     }
     const unsigned int S = (unsigned int)Y.S;
@@ -1696,15 +1784,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         return;
     }
     if (r == S) {
-        decider_role<D, kExact, kRagged>(P, bs, sm);
+        decider_role<D, kExact, kRagged, kPipe>(P, bs, sm);
         return;
     }
     r -= S + 1u;
     if (r < (unsigned int)Y.Mt) {
-        mass_role<D, kExact, kRagged>(P, bm, (int)r, sm);
+        mass_role<D, kExact, kRagged, kPipe>(P, bm, (int)r, sm);
         return;
     }
-    draw_role<D, kExact, kRagged>(P, bm, sm);
+    draw_role<D, kExact, kRagged, kPipe>(P, bm, sm);
 }
 
 // Exact mode with the row-staged early exit (see row_decider_role).  Index
@@ -1813,7 +1901,9 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     }
     const dim3 grid((unsigned int)n_total), block(kThreads);
     if (a.gammas == nullptr) {
-        if (exact)
+        if (exact && pipelined_waits(a.B, a.gamma, a.V, a.dt))
+            hipLaunchKernelGGL((verify_kernel<D, true, false, true>), grid, block, 0, a.stream, P);
+        else if (exact)
             hipLaunchKernelGGL((verify_kernel<D, true, false>), grid, block, 0, a.stream, P);
         else
             hipLaunchKernelGGL((verify_kernel<D, false, false>), grid, block, 0, a.stream, P);

@@ -342,6 +342,20 @@ static sv_status_t val(const Call& a, bool exact) {
     return validate(a, exact, &p);
 }
 
+// Which single passes wait with two polls in flight: the short streams of
+// the small workloads, not the long stream of the large one.
+static void section_pipelined_waits() {
+    CHECK(pipelined_waits(1, 5, 51865, SV_F32) && pipelined_waits(1, 10, 32000, SV_F16) &&
+              pipelined_waits(16, 5, 51865, SV_F32),
+          "short streams");
+    CHECK(!pipelined_waits(64, 8, 128256, SV_BF16) && !pipelined_waits(56, 3, 128256, SV_BF16), "long streams");
+    for (long long B : {1LL, 7LL, 64LL})
+        for (long long g : {1LL, 8LL, 128LL})
+            for (long long V : {1LL, 4097LL, 1LL << 20})
+                CHECK(pipelined_waits(B, g, V, SV_F32) == (2 * g * V * 4 * B < kLagStreamBytes), "rule");
+    printf("pipelined waits: ok\n");
+}
+
 static void section_validation() {
     const float inf = std::numeric_limits<float>::infinity();
     const float nan = std::numeric_limits<float>::quiet_NaN();
@@ -396,6 +410,7 @@ int main() {
     section_div();
     section_plans();
     section_layouts();
+    section_pipelined_waits();
     section_validation();
     printf("all checks passed (%lld)\n", g_checks);
     return 0;

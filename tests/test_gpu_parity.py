@@ -65,14 +65,14 @@ def test_full_size_workloads(name):
 # --- edge cases ---------------------------------------------------------------
 
 @pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
-@pytest.mark.parametrize("V", [1, 2, 7, 8, 63, 64, 65, 4097])
+@pytest.mark.parametrize("V", [1, 2, 7, 8, 63, 64, 65, 255, 256, 257, 4097, 8193])
 def test_vocab_edge_sizes(dtype, V):
     for gamma, B in [(1, 1), (3, 5)]:
         x = W.small_case(B, gamma, V, dtype, seed=100 + V)
         compare(x, run_gpu(x), run_oracle(x), label=f"V={V} {dtype} g={gamma}")
 
 
-@pytest.mark.parametrize("gamma", [1, 2, 5, 13, 16, 17, 20, 31, 33, 64, 65, 100, 128])
+@pytest.mark.parametrize("gamma", [1, 2, 4, 5, 6, 10, 11, 13, 16, 17, 20, 21, 31, 33, 40, 64, 65, 80, 81, 100, 128])
 def test_gamma_range(gamma):
     # the row-normaliser merge groups 16, 8, 4, 2 or 1 lanes per row by the
     # number of rows (2 gamma); low noise so that long accepted prefixes occur
@@ -85,9 +85,11 @@ def test_gamma_range(gamma):
 
 @pytest.mark.parametrize("mode", ["exact", "sigmoid"])
 def test_unaligned_rows_and_offsets(mode):
-    # odd V in fp32: every row after the first starts off a 16-byte boundary
-    x = W.small_case(7, 4, 12347, "f32", mode=mode, seed=3, alpha=-1e3, beta=1e3)
-    compare(x, run_gpu(x), run_oracle(x), label="odd V f32")
+    # odd V in fp32: every row after the first starts off a 16-byte boundary;
+    # odd V in 16-bit storage: rows start off a 4-byte boundary (element loads)
+    for dt, V in (("f32", 12347), ("bf16", 12347), ("f16", 2049)):
+        x = W.small_case(7, 4, V, dt, mode=mode, seed=3, alpha=-1e3, beta=1e3)
+        compare(x, run_gpu(x), run_oracle(x), label=f"odd V {dt}")
 
 
 @pytest.mark.parametrize("T", [0.7, 1.0, 1.3])
