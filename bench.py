@@ -47,7 +47,7 @@ def algorithmic_bytes(w, accepted_len=None) -> int:
     return w.batch * 2 * w.gamma * s + rows * w.vocab * s + small
 
 
-KERNEL_SOURCES = ("spec_verify.hip", "sv_device.hpp")
+KERNEL_SOURCES = ("spec_verify.hip", "sv_device.hpp", "plan.hpp")
 
 
 def source_hash() -> str:
@@ -315,6 +315,10 @@ def main() -> int:
                          "the sigmoid constants alpha = -beta, over a top-k mask of the logits, over ragged "
                          "per-element gamma, the exact mode's early exit against its single pass, or the decoding "
                          "loop with the gamma rule (--steps iterations)")
+    ap.add_argument("--noise", type=float, default=None,
+                    help="normal logits (scale 2) with this draft-target noise instead of the workload's own law "
+                         "(e.g. 2.0: most elements reject an early draft, so the residual path runs for nearly "
+                         "every element)")
     ap.add_argument("--copy-calibration-mb", type=float, default=0.0,
                     help="only run a plain copy of this size (for counter calibration) and exit")
     args = ap.parse_args()
@@ -333,6 +337,9 @@ def main() -> int:
     from paper_2406_11016_amd import workloads as W
 
     w = W.WORKLOADS[args.workload or W.HEADLINE]
+    if args.noise is not None:
+        w = w.with_(name=f"{w.name}_normal_noise{args.noise:g}", base="normal", base_scale=2.0,
+                    noise_scale=args.noise)
     log(f"generating {w.name} ({w.logit_bytes / 1e6:.1f} MB of logits)")
     t0 = time.perf_counter()
     x = W.generate(w)

@@ -217,9 +217,10 @@ __device__ __forceinline__ float unpack_lo(unsigned long long w) { return __uint
 // which __syncthreads would.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// Sleep between the two polls in flight of a wait (s_sleep units of 64
-// clocks: about 0.05 us; a shorter gap measured faster).
-constexpr int kPollGap = 2;
+// Sleep between the two polls in flight of a wait, in s_sleep units of 64
+// clocks: none (gaps of 1, 2 and 4 units, and the 10 of a first version,
+// measured slower: the second poll is best issued at once).
+constexpr int kPollGap = 0;
 
 // Waits until the n words at p are published, handing each to take(i, w)
 // (w the raw, still inverted word).  Called by every thread; returns false
@@ -289,11 +290,11 @@ __device__ __forceinline__ bool poll_at(int n, A addr, F take, int limit) {
     };
     issue(a);
     for (int round = 0;; round += 2) {
-        __builtin_amdgcn_s_sleep(kPollGap);
+        if constexpr (kPollGap > 0) __builtin_amdgcn_s_sleep(kPollGap);
         issue(c);
         if (check(a, round)) return true;
         if (round + 1 >= limit) return false;
-        __builtin_amdgcn_s_sleep(kPollGap);
+        if constexpr (kPollGap > 0) __builtin_amdgcn_s_sleep(kPollGap);
         issue(a);
         if (check(c, round + 1)) return true;
         if (round + 2 >= limit) return false;
@@ -1267,7 +1268,7 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
         ka = __hip_atomic_load(words + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         sa = __hip_atomic_load(words + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         for (int spin = 0;; spin += 2) {
-            __builtin_amdgcn_s_sleep(kPollGap);
+            if constexpr (kPollGap > 0) __builtin_amdgcn_s_sleep(kPollGap);
             kb = __hip_atomic_load(words + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             sb = __hip_atomic_load(words + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (__ballot(lane < W && (ka == 0ull || sa == 0ull)) == 0ull) {
@@ -1277,7 +1278,7 @@ __device__ __forceinline__ void bonus_wave_role(const StepParams& P, int b) {
                 break;
             }
             if (spin + 1 >= limit) break;
-            __builtin_amdgcn_s_sleep(kPollGap);
+            if constexpr (kPollGap > 0) __builtin_amdgcn_s_sleep(kPollGap);
             ka = __hip_atomic_load(words + 2 * q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             sa = __hip_atomic_load(words + 2 * q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (__ballot(lane < W && (kb == 0ull || sb == 0ull)) == 0ull) {
