@@ -309,12 +309,14 @@ def main() -> int:
     ap.add_argument("--no-unfused", action="store_true", help="skip timing the unfused PyTorch comparison")
     ap.add_argument("--graph", choices=("auto", "on", "off"), default="auto",
                     help="also time the calls replayed from a HIP graph (auto: for workloads under 8 MB)")
-    ap.add_argument("--sweep", choices=("gamma", "alpha_beta", "top_k", "ragged", "early_exit", "decode_loop"),
+    ap.add_argument("--sweep", choices=("gamma", "alpha_beta", "top_k", "ragged", "early_exit", "decode_loop",
+                                        "loop_early_exit"),
                     default=None,
                     help="instead of the benchmark line: one JSON line with a sweep over gamma (1..20), over "
                          "the sigmoid constants alpha = -beta, over a top-k mask of the logits, over ragged "
                          "per-element gamma, the exact mode's early exit against its single pass, or the decoding "
-                         "loop with the gamma rule (--steps iterations)")
+                         "loop with the gamma rule (--steps iterations), or that loop at the headline shape choosing "
+                         "the early exit per step (--steps iterations)")
     ap.add_argument("--noise", type=float, default=None,
                     help="normal logits (scale 2) with this draft-target noise instead of the workload's own law "
                          "(e.g. 2.0: most elements reject an early draft, so the residual path runs for nearly "

@@ -315,6 +315,55 @@ def decode_loop(iterations: int, gamma_max: int = 20, pool: int = 32) -> dict:
                     "(spec_verify_loop_step); step_device_us only for the python loop"}
 
 
+def loop_early_exit(iterations: int, block: int = 8) -> dict:
+    """The decoding loop at the headline shape (B = 64, V = 128,256 bf16, gamma
+    held at 8: with 64 elements the gamma rule, which grows gamma only when
+    every element accepts every draft, soon keeps gamma at 1-2, where the
+    early exit has nothing to skip) over iterations alternating in blocks of `block` between the
+    headline law (most drafts accepted) and rejection-heavy logits (normal,
+    noise 2.0), with the early exit never, always, or chosen per step from the
+    previous step's acceptance ("auto"): the step's device time per iteration
+    (HIP events around the launch) in each regime."""
+    import numpy as np
+
+    from paper_2406_11016_amd import workloads as W
+    from paper_2406_11016_amd.decode_loop import DecodeLoop, SyntheticSteps
+    head = W.WORKLOADS[W.HEADLINE]
+    hi = SyntheticSteps(head, gamma_max=8, pool=2)
+    lo = SyntheticSteps(head.with_(base="normal", noise_scale=2.0), gamma_max=8, pool=2)
+    plan = [(i // block) % 2 == 0 for i in range(iterations)]      # True: the headline law
+
+    def producer(loop, i, gamma):
+        (hi if plan[i] else lo)(loop, i, gamma)
+
+    runs = []
+    for mode in ("never", "always", "auto"):
+        loop = DecodeLoop(head.batch, head.vocab, head.dtype, gamma0=8, gamma_max=8, early_exit=mode,
+                          adapt_gamma=False)
+        loop.run(producer, 2 * block)                              # warm-up
+        st = loop.run(producer, iterations, time_device=True)
+        loop.close()
+        dev = np.array(st.device_us)
+        ee = np.array(st.early_exit)
+        acc = np.array([float(np.mean(np.maximum(a, 0))) for a in st.accepted])
+        pl = np.array(plan)
+        p = {"early_exit": mode, "iterations": iterations,
+             "step_us_mean": round(float(dev.mean()), 2),
+             "step_us_headline_law": round(float(dev[pl].mean()), 2),
+             "step_us_rejection_heavy": round(float(dev[~pl].mean()), 2),
+             "early_exit_share_headline_law": round(float(ee[pl].mean()), 3),
+             "early_exit_share_rejection_heavy": round(float(ee[~pl].mean()), 3),
+             "mean_accepted_headline_law": round(float(acc[pl].mean()), 2),
+             "mean_accepted_rejection_heavy": round(float(acc[~pl].mean()), 2),
+             "mean_gamma": round(float(np.mean(st.gammas)), 2)}
+        log(json.dumps(p))
+        runs.append(p)
+    return {"sweep": "loop_early_exit", "block": block, "runs": runs,
+            "what": "decoding loop at B=64, gamma=8, V=128256 bf16; blocks of iterations alternate between the "
+                    "headline law and normal logits with noise 2.0; step_us = device time of the verification "
+                    "step per iteration"}
+
+
 def run(kind: str, steps: int, warmup: int) -> int:
     import torch
     if not torch.cuda.is_available():
@@ -333,6 +382,8 @@ def run(kind: str, steps: int, warmup: int) -> int:
         out = sweep_ragged(steps, warmup)
     elif kind == "early_exit":
         out = sweep_early_exit(steps, warmup)
+    elif kind == "loop_early_exit":
+        out = loop_early_exit(steps)
     else:
         out = decode_loop(steps)
     out["seconds"] = round(time.perf_counter() - t0, 1)

@@ -318,6 +318,16 @@ sv_status_t spec_verify_sigmoid_ragged(const void* draft_logits, const void* tar
  * to pinned memory with the outputs) and returns SV_ERR_TIMEOUT, leaving
  * *next_gamma unwritten, if it is set.
  *
+ * Early exit (exact mode; Sec. 3.1 stops at the first rejection):
+ * `early_exit` 0 runs every step through spec_verify_exact, 1 through
+ * spec_verify_exact_early_exit, 2 chooses per step from the previous step's
+ * acceptance: the early exit when the mean accepted length over the batch
+ * (sentinels counting 0) was below half of that step's gamma, the single pass
+ * otherwise and at the first step.  Both give the same outputs; the early
+ * exit is faster when most elements reject early and slower when they
+ * accept most drafts.  spec_verify_loop_last_early_exit reports the choice
+ * of the last step (1: early exit, 0: single pass, -1: no step yet).
+ *
  * Ownership: every pointer in the descriptor is the caller's and must stay
  * valid until spec_verify_loop_destroy; the loop allocates only its host
  * object, one pinned 4-byte word for the flag (at the first step) and the
@@ -325,8 +335,8 @@ sv_status_t spec_verify_sigmoid_ragged(const void* draft_logits, const void* tar
  * spec_verify_workspace_bytes(batch, g, vocab, dtype) for every g up to
  * gamma_max (zero-filled before the first iteration; each iteration leaves it
  * zero-filled).  One loop must not be stepped from two threads at once.
- * Errors: SV_ERR_NULL, SV_ERR_SHAPE, SV_ERR_PARAM (mode not 0/1, gamma out
- * of 1 .. gamma_max), SV_ERR_WORKSPACE, SV_ERR_ALLOC at creation; the
+ * Errors: SV_ERR_NULL, SV_ERR_SHAPE, SV_ERR_PARAM (mode not 0/1, early_exit
+ * not 0-2, gamma out of 1 .. gamma_max), SV_ERR_WORKSPACE, SV_ERR_ALLOC at creation; the
  * verification's own errors, SV_ERR_HIP and SV_ERR_TIMEOUT at a step.
  */
 typedef struct sv_loop sv_loop;
@@ -346,12 +356,14 @@ typedef struct sv_loop_desc {
     void* workspace;
     size_t workspace_bytes;
     hipStream_t stream;
-    int32_t use_graphs;           /* nonzero: one captured graph per gamma */
+    int32_t use_graphs;           /* nonzero: one captured graph per gamma (and entry point) */
+    int32_t early_exit;           /* exact mode: 0 never, 1 always, 2 from the previous step's acceptance */
 } sv_loop_desc_t;
 
 sv_status_t spec_verify_loop_create(const sv_loop_desc_t* desc, sv_loop** loop);
 sv_status_t spec_verify_loop_step(sv_loop* loop, int32_t gamma, int32_t* next_gamma);
 sv_status_t spec_verify_loop_destroy(sv_loop* loop);
+int32_t spec_verify_loop_last_early_exit(const sv_loop* loop);
 
 /* Static description of a status code. */
 const char* spec_verify_status_string(sv_status_t status);

@@ -40,6 +40,7 @@ SYMBOLS = (
     "spec_verify_loop_create",
     "spec_verify_loop_step",
     "spec_verify_loop_destroy",
+    "spec_verify_loop_last_early_exit",
     "spec_verify_status_string",
 )
 
@@ -63,7 +64,7 @@ class LoopDesc(ctypes.Structure):
                 ("target", ctypes.c_void_p), ("tokens", ctypes.c_void_p), ("uniforms", ctypes.c_void_p),
                 ("accepted_len", ctypes.c_void_p), ("next_token", ctypes.c_void_p), ("host_out", ctypes.c_void_p),
                 ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t), ("stream", ctypes.c_void_p),
-                ("use_graphs", ctypes.c_int32)]
+                ("use_graphs", ctypes.c_int32), ("early_exit", ctypes.c_int32)]
 
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
@@ -112,6 +113,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.spec_verify_loop_step.restype = ctypes.c_int
     lib.spec_verify_loop_destroy.argtypes = [_vp]
     lib.spec_verify_loop_destroy.restype = ctypes.c_int
+    lib.spec_verify_loop_last_early_exit.argtypes = [_vp]
+    lib.spec_verify_loop_last_early_exit.restype = ctypes.c_int32
     lib.spec_verify_status_string.argtypes = [ctypes.c_int]
     lib.spec_verify_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -341,6 +344,11 @@ def loop_step(handle: ctypes.c_void_p, gamma: int) -> int:
     nxt = ctypes.c_int32()
     _check(load_library().spec_verify_loop_step(handle, int(gamma), ctypes.byref(nxt)), "spec_verify_loop_step")
     return int(nxt.value)
+
+
+def loop_last_early_exit(handle: ctypes.c_void_p) -> int:
+    """Whether the native loop's last step ran the early exit (1), the single pass (0), or no step yet (-1)."""
+    return int(load_library().spec_verify_loop_last_early_exit(handle))
 
 
 def loop_destroy(handle: ctypes.c_void_p) -> None:

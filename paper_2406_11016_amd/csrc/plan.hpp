@@ -350,6 +350,15 @@ inline long long staged_workgroups(long long B, long long gamma, long long V, sv
     return n;
 }
 
+// The decoding loop's automatic choice of the early exit for the next step:
+// after a step of `gamma` drafts whose accepted lengths sum to `accepted_sum`
+// over B elements, the early exit pays when the mean accepted length is below
+// gamma / 2 (it measured 1.24-1.48x the single pass at mean accepted 1.23 ..
+// 0.02 of gamma 8, and 0.78x at 7.41).
+inline bool early_exit_pays(long long accepted_sum, long long B, int gamma) {
+    return B > 0 && 2 * accepted_sum < (long long)gamma * B;
+}
+
 // ---------------------------------------------------------------------------
 // Arguments of one call and their validation (before anything is launched).
 // ---------------------------------------------------------------------------

@@ -20,6 +20,13 @@ accepted length to decide the next gamma and which tokens to append.  With
 ``use_graphs`` the call for each gamma is captured once into a HIP graph
 (lazily, on first use) and replayed instead; on ROCm 7 that measured slower
 than launching this one-kernel step directly, so it is off by default.
+
+In the exact mode ``early_exit`` picks the entry point of each step:
+``"never"`` (the single pass), ``"always"`` (the early exit, which stops
+streaming an element's rows at its first rejection, Sec. 3.1) or ``"auto"``:
+the early exit when the previous step's mean accepted length was below half
+of its gamma, the single pass otherwise and at the first step.  Both give
+the same outputs.
 """
 from __future__ import annotations
 
@@ -42,6 +49,16 @@ def next_gamma(gamma: int, accepted: np.ndarray, gamma_max: int, grow: int = 2, 
     return max(gamma - shrink, 1)
 
 
+EARLY_EXIT_CODES = {"never": 0, "always": 1, "auto": 2}
+
+
+def early_exit_pays(accepted: np.ndarray, gamma: int) -> bool:
+    """The automatic choice for the next step: the early exit when the mean
+    accepted length of the last step (sentinels counting 0) was below half
+    of its gamma (the native loop's rule, early_exit_pays in plan.hpp)."""
+    return accepted.size > 0 and 2 * int(np.sum(np.maximum(accepted, 0))) < gamma * accepted.size
+
+
 @dataclass
 class LoopStats:
     iterations: int = 0
@@ -50,6 +67,7 @@ class LoopStats:
     accepted: List[np.ndarray] = field(default_factory=list)
     next_tokens: List[np.ndarray] = field(default_factory=list)
     device_us: List[float] = field(default_factory=list)   # per iteration, when timed
+    early_exit: List[bool] = field(default_factory=list)   # per iteration: the early exit ran
 
 
 class DecodeLoop:
@@ -57,9 +75,17 @@ class DecodeLoop:
 
     def __init__(self, batch: int, vocab: int, dtype: str, *, mode: str = "exact", temperature: float = 1.0,
                  alpha: float = -1.0e4, beta: float = 1.0e4, gamma0: int = 5, gamma_max: int = 20,
-                 use_graphs: bool = False, native: bool = False, device="cuda"):
+                 use_graphs: bool = False, native: bool = False, early_exit: str = "never",
+                 adapt_gamma: bool = True, device="cuda"):
         if not (1 <= gamma0 <= gamma_max):
             raise ValueError("need 1 <= gamma0 <= gamma_max")
+        if early_exit not in EARLY_EXIT_CODES:
+            raise ValueError(f"early_exit must be one of {sorted(EARLY_EXIT_CODES)}")
+        if native and not adapt_gamma:
+            raise ValueError("the native loop always applies the gamma rule")
+        self.early_exit = early_exit
+        self.adapt_gamma = adapt_gamma   # False: every iteration verifies gamma0 drafts (measurements)
+        self._early_next = mode == "exact" and early_exit == "always"
         self.B, self.V, self.dtype, self.mode = batch, vocab, dtype, mode
         self.temperature, self.alpha, self.beta = temperature, alpha, beta
         self.gamma0, self.gamma_max, self.use_graphs = gamma0, gamma_max, use_graphs
@@ -77,7 +103,7 @@ class DecodeLoop:
         ws = max(binding.workspace_bytes(B, g, V, tdt) for g in range(1, G + 1))
         self.ws = torch.zeros((ws + 15) // 16 * 16, dtype=torch.uint8, device=self.device)
         self.stream = torch.cuda.Stream(self.device)
-        self.graphs: Dict[int, torch.cuda.CUDAGraph] = {}
+        self.graphs: Dict[Tuple[int, bool], torch.cuda.CUDAGraph] = {}
         # the native loop: one library call per iteration (graph replay or
         # launch, the copies to pinned memory, the wait and the gamma rule)
         self.native = None
@@ -88,7 +114,7 @@ class DecodeLoop:
                 target=self.target.data_ptr(), tokens=self.tokens.data_ptr(), uniforms=self.uniforms.data_ptr(),
                 accepted_len=self.acc.data_ptr(), next_token=self.nxt.data_ptr(), host_out=self.host.data_ptr(),
                 workspace=self.ws.data_ptr(), workspace_bytes=self.ws.numel(), stream=self.stream.cuda_stream,
-                use_graphs=1 if use_graphs else 0)
+                use_graphs=1 if use_graphs else 0, early_exit=EARLY_EXIT_CODES[early_exit])
             self.native = binding.loop_create(desc)
 
     def close(self) -> None:
@@ -112,22 +138,23 @@ class DecodeLoop:
         return (self.draft[:B * gamma * V].view(B, gamma, V), self.target[:B * (gamma + 1) * V].view(B, gamma + 1, V),
                 self.tokens[:B * gamma].view(B, gamma), self.uniforms[:B * (gamma + 1)].view(B, gamma + 1))
 
-    def _call(self, gamma: int) -> None:
+    def _call(self, gamma: int, early: bool = False) -> None:
         d, t, tok, u = self.views(gamma)
         binding.verify(d, t, tok, u, mode=self.mode, temperature=self.temperature, alpha=self.alpha,
-                       beta=self.beta, accepted_len=self.acc, next_token=self.nxt, workspace=self.ws)
+                       beta=self.beta, accepted_len=self.acc, next_token=self.nxt, workspace=self.ws,
+                       early_exit=early)
 
-    def _graph(self, gamma: int) -> torch.cuda.CUDAGraph:
-        g = self.graphs.get(gamma)
+    def _graph(self, gamma: int, early: bool = False) -> torch.cuda.CUDAGraph:
+        g = self.graphs.get((gamma, early))
         if g is None:
             with torch.cuda.stream(self.stream):
-                self._call(gamma)          # eager once on the capture stream (checks the arguments)
+                self._call(gamma, early)   # eager once on the capture stream (checks the arguments)
             self.stream.synchronize()
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=self.stream):
-                self._call(gamma)
+                self._call(gamma, early)
             self.stream.synchronize()
-            self.graphs[gamma] = g
+            self.graphs[(gamma, early)] = g
         return g
 
     def capture_all(self) -> None:
@@ -135,18 +162,19 @@ class DecodeLoop:
         if self.native is not None:
             return
         for g in range(1, self.gamma_max + 1):
-            self._graph(g)
+            for early in ((False, True) if self.mode == "exact" and self.early_exit != "never" else (False,)):
+                self._graph(g, early)
 
     # -- one iteration ---------------------------------------------------------
-    def launch(self, gamma: int) -> None:
+    def launch(self, gamma: int, early: bool = False) -> None:
         """Enqueue the verification of the buffers' current contents on the loop's stream."""
         if self.use_graphs:
-            graph = self._graph(gamma)
+            graph = self._graph(gamma, early)
             with torch.cuda.stream(self.stream):
                 graph.replay()
         else:
             with torch.cuda.stream(self.stream):
-                self._call(gamma)
+                self._call(gamma, early)
 
     def collect(self) -> Tuple[np.ndarray, np.ndarray]:
         """Wait for the launched call; its accepted lengths and next tokens."""
@@ -183,6 +211,7 @@ class DecodeLoop:
                 nxt_gamma = binding.loop_step(self.native, gamma)
                 h = self.host.numpy()
                 L, nx = h[:self.B].copy(), h[self.B:].copy()
+                stats.early_exit.append(binding.loop_last_early_exit(self.native) == 1)
                 stats.iterations += 1
                 stats.gammas.append(gamma)
                 stats.accepted.append(L)
@@ -190,12 +219,16 @@ class DecodeLoop:
                 stats.tokens += int(np.sum(np.where(L >= 0, L + 1, 0)))
                 gamma = nxt_gamma
                 continue
+            early = self._early_next
             if ev is not None:
                 ev[0].record(self.stream)
-            self.launch(gamma)
+            self.launch(gamma, early)
             if ev is not None:
                 ev[1].record(self.stream)
             L, nx = self.collect()
+            stats.early_exit.append(early)
+            if self.mode == "exact" and self.early_exit == "auto":
+                self._early_next = early_exit_pays(L, gamma)
             if ev is not None:
                 stats.device_us.append(ev[0].elapsed_time(ev[1]) * 1000.0)
             stats.iterations += 1
@@ -203,7 +236,8 @@ class DecodeLoop:
             stats.accepted.append(L)
             stats.next_tokens.append(nx)
             stats.tokens += int(np.sum(np.where(L >= 0, L + 1, 0)))
-            gamma = next_gamma(gamma, L, self.gamma_max)
+            if self.adapt_gamma:
+                gamma = next_gamma(gamma, L, self.gamma_max)
         return stats
 
 

@@ -356,6 +356,19 @@ static void section_pipelined_waits() {
     printf("pipelined waits: ok\n");
 }
 
+// The decoding loop's automatic early exit: below half of gamma accepted on
+// average (hand-worked cases, the same as the Python loop's tests).
+static void section_loop_early_exit() {
+    CHECK(early_exit_pays(11, 4, 8), "mean 2.75 < 4");
+    CHECK(!early_exit_pays(16, 4, 8), "mean 4 is not below 4");
+    CHECK(!early_exit_pays(24, 4, 8), "mean 6");
+    CHECK(early_exit_pays(0, 64, 1), "nothing accepted at gamma 1");
+    CHECK(!early_exit_pays(32, 64, 1), "half accepted at gamma 1");
+    CHECK(early_exit_pays(31, 64, 1), "just under half");
+    CHECK(!early_exit_pays(0, 0, 8), "empty batch");
+    printf("loop early exit: ok\n");
+}
+
 static void section_validation() {
     const float inf = std::numeric_limits<float>::infinity();
     const float nan = std::numeric_limits<float>::quiet_NaN();
@@ -411,6 +424,7 @@ int main() {
     section_plans();
     section_layouts();
     section_pipelined_waits();
+    section_loop_early_exit();
     section_validation();
     printf("all checks passed (%lld)\n", g_checks);
     return 0;

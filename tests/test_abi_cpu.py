@@ -206,6 +206,8 @@ def test_loop_create_checks(lib):
     for field in ("draft", "target", "tokens", "uniforms", "accepted_len", "next_token", "host_out", "workspace"):
         assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(**{field: None})), ctypes.byref(h)) == SV_ERR_NULL
     assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(mode=2)), ctypes.byref(h)) == SV_ERR_PARAM
+    for bad in (-1, 3):
+        assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(early_exit=bad)), ctypes.byref(h)) == SV_ERR_PARAM
     assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(gamma_max=0)), ctypes.byref(h)) == SV_ERR_SHAPE
     assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(gamma_max=129)), ctypes.byref(h)) == SV_ERR_SHAPE
     need = max(lib.spec_verify_workspace_bytes(2, g, 100, 0) for g in range(1, 7))
@@ -213,6 +215,8 @@ def test_loop_create_checks(lib):
                                        ctypes.byref(h)) == SV_ERR_WORKSPACE
     # a valid descriptor: the host object only (graphs come with the first step)
     assert lib.spec_verify_loop_create(ctypes.byref(_loop_desc(workspace_bytes=need)), ctypes.byref(h)) == 0
+    assert lib.spec_verify_loop_last_early_exit(h) == -1      # no step yet
+    assert lib.spec_verify_loop_last_early_exit(None) == -1
     nxt = ctypes.c_int32()
     assert lib.spec_verify_loop_step(h, 0, ctypes.byref(nxt)) == SV_ERR_PARAM
     assert lib.spec_verify_loop_step(h, 7, ctypes.byref(nxt)) == SV_ERR_PARAM

@@ -35,3 +35,18 @@ def test_trajectory():
         seen.append(gamma)
         gamma = next_gamma(gamma, np.array([min(L, gamma)]), 20)
     assert seen == [5, 7, 9, 8, 7, 6, 5, 4, 3, 2]
+
+
+def test_early_exit_choice_rule():
+    """The loop's automatic early exit: below half of gamma accepted on
+    average, sentinels counting 0 (the same hand-worked cases as the native
+    rule's check in tests/native/plan_check.cpp)."""
+    from paper_2406_11016_amd.decode_loop import early_exit_pays
+    assert early_exit_pays(np.array([2, 3, 3, 3]), 8)          # mean 2.75 < 4
+    assert not early_exit_pays(np.array([4, 4, 4, 4]), 8)      # mean 4 is not below 4
+    assert not early_exit_pays(np.array([6, 6, 6, 6]), 8)
+    assert early_exit_pays(np.zeros(64, dtype=np.int32), 1)
+    assert not early_exit_pays(np.array([1] * 32 + [0] * 32), 1)
+    assert early_exit_pays(np.array([1] * 31 + [0] * 33), 1)
+    assert early_exit_pays(np.array([-1, -1, 8, 0]), 8)        # sentinels count 0: mean 2
+    assert not early_exit_pays(np.array([], dtype=np.int32), 8)

@@ -75,3 +75,60 @@ def test_decode_loop_matches_oracle_and_rule(case):
         assert np.array_equal(st.next_tokens[i][ok], o.next_token[ok]), (i, g, st.next_tokens[i], o.next_token)
     print(f"[loop] {case}: gammas {st.gammas[:20]}... grew {grew} shrank {shrank} tokens {st.tokens}", flush=True)
     assert grew >= 1
+
+
+def test_decode_loop_chooses_the_early_exit_from_the_last_acceptance():
+    """The headline shape (B = 64, V = 128,256 bf16, gamma up to 8, where the
+    early exit's staged order applies), iterations alternating between the
+    headline law (most drafts accepted) and rejection-heavy logits (normal,
+    noise 2.0: most elements reject an early draft).  With early_exit="auto"
+    a step runs the early exit exactly when the previous step's mean accepted
+    length was below half of its gamma (the first step never); "always" and
+    "never" run one entry point throughout.  Every run, Python or native,
+    gives the same outputs, and those are the oracle's."""
+    head = W.WORKLOADS[W.HEADLINE]
+    hi = SyntheticSteps(head, gamma_max=8, pool=1)
+    lo = SyntheticSteps(head.with_(base="normal", noise_scale=2.0), gamma_max=8, pool=1)
+    plan = [True, True, False, False, True, False]   # True: the headline law
+
+    def producer(loop, i, gamma):
+        (hi if plan[i] else lo)(loop, i, gamma)
+
+    runs = {}
+    for native in (False, True):
+        for mode in ("auto", "always", "never"):
+            loop = DecodeLoop(head.batch, head.vocab, head.dtype, gamma0=8, gamma_max=8, native=native,
+                              early_exit=mode)
+            try:
+                runs[(native, mode)] = loop.run(producer, len(plan))
+            finally:
+                loop.close()
+            torch.cuda.synchronize()
+    ref = runs[(False, "never")]
+    for key, st in runs.items():
+        assert st.gammas == ref.gammas, key
+        for a, b in zip(st.accepted, ref.accepted):
+            assert np.array_equal(a, b), key
+        for a, b in zip(st.next_tokens, ref.next_tokens):
+            assert np.array_equal(a, b), key
+        mode = key[1]
+        if mode != "auto":
+            assert st.early_exit == [mode == "always"] * len(plan), key
+            continue
+        assert st.early_exit[0] is False, key
+        for i in range(1, len(plan)):
+            L, g = st.accepted[i - 1], st.gammas[i - 1]
+            assert st.early_exit[i] == (2 * int(np.sum(np.maximum(L, 0))) < g * L.size), (key, i)
+    # the regimes: after a headline-law step the single pass, after a
+    # rejection-heavy one the early exit
+    auto = runs[(True, "auto")]
+    for i in range(1, len(plan)):
+        assert auto.early_exit[i] == (not plan[i - 1]), (i, [float(np.mean(a)) for a in auto.accepted])
+    for i in range(len(plan)):
+        x = (hi if plan[i] else lo).host_inputs(i, ref.gammas[i])
+        o = run_oracle(x)
+        ok = ~o.flagged(1e-6)
+        assert np.array_equal(ref.accepted[i][ok], o.accepted_len[ok]), i
+        assert np.array_equal(ref.next_tokens[i][ok], o.next_token[ok]), i
+    print(f"[loop early exit] gammas {ref.gammas} mean accepted "
+          f"{[round(float(np.mean(a)), 2) for a in ref.accepted]} auto {auto.early_exit}", flush=True)
