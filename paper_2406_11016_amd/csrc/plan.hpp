@@ -47,6 +47,9 @@ constexpr size_t kErrorFlagOffset = 4;
 constexpr size_t kSpinLimitOffset = 8;
 
 inline long long ceil_div(long long a, long long b) { return (a + b - 1) / b; }
+
+// XCDs of the GPU: workgroup i of a launch runs on XCD i mod kXcds (see g_tile).
+constexpr int kXcds = 8;
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 inline bool valid_dtype(sv_dtype_t dt) { return dt == SV_F32 || dt == SV_F16 || dt == SV_BF16; }
@@ -214,6 +217,39 @@ struct Role {
     int k;      // stats: chunk of the slot; row gamma: tile; mass: tile
 };
 
+// Target row gamma's tiles (segment G of the single pass).  Workgroup i of a
+// launch runs on XCD i mod kXcds (the dispatcher deals workgroups to the XCDs
+// in turn), and each XCD has its own L2, so a workgroup re-reads data that
+// another workgroup of its XCD loaded from that L2 (about a quarter of the
+// latency of HBM).  The elements are taken in groups of kXcds: in a full
+// group, tile j of the group's element e sits at position
+// kXcds j + (e + d) mod kXcds of the group, d = (end2 - end1) mod kXcds, so
+// that every tile of element b runs on the XCD of b's bonus workgroup (id
+// end2 + b), whose draw re-reads one of their quarters.  The elements of a
+// last partial group keep their tiles contiguous.
+struct GTile {
+    int b;  // batch element
+    int k;  // tile of its target row gamma
+};
+
+// Tile t of segment G: dcg divides by nchunkg, and end1 / end2 are the
+// layout's.  Scalar arguments and forced inlining keep the kernel's launch
+// arguments in registers (a call would spill around it).
+__attribute__((always_inline)) constexpr GTile g_tile(Div dcg, unsigned int end1, unsigned int end2, int B, int nchunkg,
+                                                      int t) {
+    static_assert(kXcds == 8, "the masks below take kXcds = 8");
+    const int bfull = B & ~7;
+    if (t < bfull * nchunkg) {
+        const int g = (int)div_of(dcg, (unsigned int)t >> 3);
+        const int p = t - g * 8 * nchunkg;
+        const int d = (int)((end2 - end1) & 7u);
+        return GTile{8 * g + (((p & 7) - d) & 7), p >> 3};
+    }
+    const int t2 = t - bfull * nchunkg;
+    const int bb = (int)div_of(dcg, (unsigned int)t2);
+    return GTile{bfull + bb, t2 - bb * nchunkg};
+}
+
 // The role of workgroup `id` of the single-pass launch (id < end2 + B).
 constexpr Role role_at(const Layout& y, int nchunk1, int nchunkg, unsigned int id) {
     unsigned int r = 0;
@@ -229,9 +265,8 @@ constexpr Role role_at(const Layout& y, int nchunk1, int nchunkg, unsigned int i
         bs = y.lagM + (int)k;
         bm = (int)k;
     } else if (id < y.endg) {
-        const int t = (int)(id - y.end1);
-        const int b = (int)div_of(y.dcg, (unsigned int)t);
-        return Role{kRoleRowG, b, 0, t - b * nchunkg};
+        const GTile g = g_tile(y.dcg, y.end1, y.end2, y.b2 + y.lagM, nchunkg, (int)(id - y.end1));
+        return Role{kRoleRowG, g.b, 0, g.k};
     } else if (id < y.end2) {
         const unsigned int loc = id - y.endg;
         const unsigned int k = div_of(y.d2, loc);

@@ -1762,12 +1762,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         bs = Y.lagM + (int)k;
         bm = (int)k;
     } else if (id < Y.endg) {
-        const int t = (int)(id - Y.end1);
-        const int b = (int)div_of(Y.dcg, (unsigned int)t);
+        const GTile g = g_tile(Y.dcg, Y.end1, Y.end2, P.B, P.nchunkg, (int)(id - Y.end1));
         if (kExact)
-            stats_role<D, kRagged>(P, b, 2 * P.gamma, t - b * P.nchunkg, sm);
+            stats_role<D, kRagged>(P, g.b, 2 * P.gamma, g.k, sm);
         else
-            sigmoid_row_role<D, kRagged>(P, b, t - b * P.nchunkg);
+            sigmoid_row_role<D, kRagged>(P, g.b, g.k);
         return;
     } else if (id < Y.end2) {
         const unsigned int loc = id - Y.endg;

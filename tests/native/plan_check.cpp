@@ -11,7 +11,8 @@
 //   3. Both launch layouts simulated workgroup by workgroup (role_at,
 //      staged_role_at): every role of every element appears exactly once, and
 //      every workgroup that waits comes after the workgroups it waits on (the
-//      ordering the kernels' deadlock-freedom rests on).
+//      ordering the kernels' deadlock-freedom rests on); target row gamma's
+//      tiles of an element share its bonus workgroup's XCD (id mod 8).
 //   4. Argument validation: the cases of the C ABI's error contract.
 //
 // Prints one line per section and exits nonzero on the first failure.
@@ -197,6 +198,10 @@ static void simulate_single_pass(int B, int gamma, int V, sv_dtype_t dt, bool ex
         for (int k = 0; k < p.nchunkg; ++k) {
             const long long t = s.rowg[(size_t)b * p.nchunkg + k];
             CHECK(t >= 0 && t < s.bonus[b], "row gamma tile %d of element %d", k, b);
+            // in a full group of kXcds elements, on the XCD of the element's bonus workgroup
+            if (b < (B & ~(kXcds - 1)))
+                CHECK(t % kXcds == s.bonus[b] % kXcds, "row gamma tile %d of element %d: XCD %lld, bonus %lld", k, b,
+                      t % kXcds, s.bonus[b] % kXcds);
         }
         for (int k = 0; k < p.nchunk2; ++k) {
             const long long t = s.mass[(size_t)b * p.nchunk2 + k];
