@@ -76,19 +76,28 @@ __device__ __forceinline__ float expm1_small(float x) {
 // and Lambda = k + log2(s) from the row normaliser.  The residual
 // a(x) = max(0, p - q) (eqs. (2)-(3)) is formed as q (2^d - 1) with
 // d = log2 p(x) - log2 q(x), so p == q cancels exactly and small differences
-// keep their relative precision.
+// keep their relative precision.  kFlat evaluates both forms and selects
+// (the same values, without a divergent branch per element: quicker where a
+// workgroup's chain is the step's critical path, slower where the residual
+// pass shares the GPU with the stream and most weights are 0).
 struct ExactWeights {
     int kind;
     float c;
     float kp, lp_hi, lp_lo;  // target row: reference k and log2(s) as hi + lo
     float kq, lq_hi, lq_lo;  // draft row
     float d_hi, d_lo;        // Lambda_p - Lambda_q as hi + lo
-    template <int KIND>
+    template <int KIND, bool kFlat = false>
     __device__ __forceinline__ float eval(float zp, float zq) const {
         if (KIND == kTargetRow) return exp2_hw((fmaf(zp, c, -kp) - lp_hi) - lp_lo);
         float dz, dz_lo;
         two_diff(zp, zq, dz, dz_lo);
         const float d = fmaf(dz_lo, c, fmaf(dz, c, -d_hi)) - d_lo;
+        if constexpr (kFlat) {
+            const float q = exp2_hw((fmaf(zq, c, -kq) - lq_hi) - lq_lo);
+            const float near = q * expm1_small(d * kLn2);
+            const float far = exp2_hw((fmaf(zp, c, -kp) - lp_hi) - lp_lo) - q;
+            return (d > 0.0f) ? ((d <= 0.5f) ? near : far) : 0.0f;  // NaN d: 0
+        }
         if (!(d > 0.0f)) return 0.0f;
         const float q = exp2_hw((fmaf(zq, c, -kq) - lq_hi) - lq_lo);
         if (d <= 0.5f) return q * expm1_small(d * kLn2);
@@ -107,7 +116,7 @@ __device__ __forceinline__ float sigm(float x) {
 struct SigmoidWeights {
     int kind;
     float s, s0;  // u = fma(z, s, s0)
-    template <int KIND>
+    template <int KIND, bool kFlat = false>
     __device__ __forceinline__ float eval(float zp, float zq) const {
         const float up = fmaf(zp, s, s0);
         if (KIND == kTargetRow) return sigm(up);
@@ -353,7 +362,7 @@ __device__ __forceinline__ Span sub_chunk(int k2, int w, int chunk2, int V, int 
 // start, n elements); optionally stores every weight.  Valid in every lane.
 // Lanes take vectors lane, lane + 64, ...; kPassUnroll 16-byte loads per row
 // are in flight per lane, kept raw and unpacked one vector at a time.
-template <class D, int KIND, class W>
+template <class D, int KIND, bool kFlat, class W>
 __device__ __forceinline__ double wave_weight_sum_k(const typename D::T* rp, const typename D::T* rq, int n,
                                                     const W& w, float* wout) {
     constexpr int E = D::E;
@@ -386,7 +395,7 @@ __device__ __forceinline__ double wave_weight_sum_k(const typename D::T* rp, con
             }
 #pragma unroll
             for (int e = 0; e < E; ++e) {
-                const float a = w.template eval<KIND>(zp[e], two_rows ? zq[e] : -INFINITY);
+                const float a = w.template eval<KIND, kFlat>(zp[e], two_rows ? zq[e] : -INFINITY);
                 if (wout != nullptr && v * E + e < n) wout[v * E + e] = a;
                 acc += (double)a;
             }
@@ -395,11 +404,11 @@ __device__ __forceinline__ double wave_weight_sum_k(const typename D::T* rp, con
     return wave_sum(acc);
 }
 
-template <class D, class W>
+template <class D, bool kFlat = false, class W>
 __device__ double wave_weight_sum(const typename D::T* rp, const typename D::T* rq, int n, const W& w,
                                   float* wout) {
-    return (w.kind == kTargetRow) ? wave_weight_sum_k<D, kTargetRow>(rp, rq, n, w, wout)
-                                  : wave_weight_sum_k<D, kResidual>(rp, rq, n, w, wout);
+    return (w.kind == kTargetRow) ? wave_weight_sum_k<D, kTargetRow, kFlat>(rp, rq, n, w, wout)
+                                  : wave_weight_sum_k<D, kResidual, kFlat>(rp, rq, n, w, wout);
 }
 
 // Lowest thread index whose predicate holds, or kThreads.  Valid in every thread.
@@ -421,7 +430,7 @@ __device__ __forceinline__ int block_first(bool pred, int* iscratch /* [kWaves] 
 // sub-chunk total at or below t.  Thread i holds vectors i NV .. i NV + NV - 1
 // (n <= kThreads * NV * E), so one workgroup scan follows element order.
 // Valid in every thread.
-template <class D, int KIND, int NV, class W>
+template <class D, int KIND, int NV, bool kFlat, class W>
 __device__ __forceinline__ int sub_chunk_find_k(const typename D::T* rp, const typename D::T* rq, int n,
                                                 const W& w, double t, double* scratch, double* incl_s,
                                                 int* iscratch, int* result) {
@@ -438,7 +447,7 @@ __device__ __forceinline__ int sub_chunk_find_k(const typename D::T* rp, const t
     for (int u = 0; u < NV; ++u)
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            a[u * E + e] = w.template eval<KIND>(zp[u][e], zq[u][e]);
+            a[u * E + e] = w.template eval<KIND, kFlat>(zp[u][e], zq[u][e]);
             sum += (double)a[u * E + e];
         }
     if (tid == 0) *result = -1;
@@ -478,11 +487,12 @@ __device__ __forceinline__ int sub_chunk_find_k(const typename D::T* rp, const t
     return *result;
 }
 
-template <class D, class W>
+template <class D, bool kFlat = false, class W>
 __device__ int sub_chunk_find(const typename D::T* rp, const typename D::T* rq, int n, const W& w, double t,
                               double* scratch, double* incl_s, int* iscratch, int* result) {
-    return (w.kind == kTargetRow) ? sub_chunk_find_k<D, kTargetRow, 1>(rp, rq, n, w, t, scratch, incl_s, iscratch, result)
-                                  : sub_chunk_find_k<D, kResidual, 1>(rp, rq, n, w, t, scratch, incl_s, iscratch, result);
+    return (w.kind == kTargetRow)
+               ? sub_chunk_find_k<D, kTargetRow, 1, kFlat>(rp, rq, n, w, t, scratch, incl_s, iscratch, result)
+               : sub_chunk_find_k<D, kResidual, 1, kFlat>(rp, rq, n, w, t, scratch, incl_s, iscratch, result);
 }
 
 // ---------------------------------------------------------------------------
@@ -1414,7 +1424,7 @@ __device__ __forceinline__ void bonus_role(const StepParams& P, int b, Smem& sm)
             const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + gb) * V + begin;
             // scan on the quarter's own scale 2^K: its largest weight is at
             // least 1/2, so a quarter with positive mass has a positive weight
-            const int local = sub_chunk_find_k<D, kTargetRow, 1>(
+            const int local = sub_chunk_find_k<D, kTargetRow, 1, false>(
                 rp, rp, n, BonusWeights<kExact>::of(P, sm.K[j]), ldexp(t_local, exp_delta(km - sm.K[j])),
                 sm.scratch, sm.incl, sm.iscratch, &sm.result);
             idx = (local >= 0) ? begin + local : -1;
@@ -1474,7 +1484,7 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
         const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V + sp.begin;
         const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V + sp.begin;
         float* wout = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V + sp.begin : nullptr;
-        m = kExact ? wave_weight_sum<D>(rp, rq, sp.n, d.ew, wout) : wave_weight_sum<D>(rp, rq, sp.n, d.sw, wout);
+        m = kExact ? wave_weight_sum<D, kPipe>(rp, rq, sp.n, d.ew, wout) : wave_weight_sum<D>(rp, rq, sp.n, d.sw, wout);
     }
     if (lane == 0) publish(P.mslot + ((size_t)b * P.nchunk2 + k2) * kWaves + wave, m);
 }
@@ -1535,7 +1545,7 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
                     const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
                     double m = 0.0;
                     if (sp.n > 0)
-                        m = kExact ? wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, wrow ? wrow + sp.begin : nullptr)
+                        m = kExact ? wave_weight_sum<D, kPipe>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, wrow ? wrow + sp.begin : nullptr)
                                    : wave_weight_sum<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, wrow ? wrow + sp.begin : nullptr);
                     if (lane == 0) sm.sub[k2 * kWaves + wave] = m;
                 }
@@ -1550,7 +1560,7 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
             break;
         }
         const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunk2, V, E);
-        const int local = kExact ? sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result)
+        const int local = kExact ? sub_chunk_find<D, kPipe>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result)
                                  : sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result);
         idx = (local >= 0) ? sp.begin + local : -1;
         if (idx < 0) bad = true;
