@@ -495,6 +495,61 @@ __device__ int sub_chunk_find(const typename D::T* rp, const typename D::T* rq, 
                : sub_chunk_find_k<D, kResidual, 1, kFlat>(rp, rq, n, w, t, scratch, incl_s, iscratch, result);
 }
 
+// sub_chunk_find by one wave when the sub-chunk has at most kWave vectors:
+// lane i holds vector i, as thread i does there, with the same sums, scan and
+// crossing rule, so the same index, without the workgroup barriers.  Valid in
+// every lane of the calling wave.
+template <class D, int KIND, bool kFlat, class W>
+__device__ __forceinline__ int wave_sub_chunk_find_k(const typename D::T* rp, const typename D::T* rq, int n,
+                                                     const W& w, double t) {
+    constexpr int E = D::E;
+    constexpr bool two_rows = (KIND == kResidual);
+    const int lane = threadIdx.x % kWave;
+    const bool fast = pair_aligned<D>(rp, rq, two_rows);
+    float zp[1][E], zq[1][E];
+    load_pair_u<D, 1>(rp, rq, two_rows, fast, lane, 1, n, zp, zq);
+    float a[E];
+    double sum = 0.0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        a[e] = w.template eval<KIND, kFlat>(zp[0][e], zq[0][e]);
+        sum += (double)a[e];
+    }
+    const double incl = wave_inclusive_scan(sum);
+    const unsigned long long over = __ballot(incl > t);
+    if (over) {
+        const int f = __ffsll((long long)over) - 1;
+        const double before = (f == 0) ? 0.0 : lane_f64(incl, f - 1);
+        int mine = -1;
+        if (lane == f) {
+            double cum = before;
+            int idx = -1, lastp = -1;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                if (a[e] > 0.0f) lastp = e;
+                cum += (double)a[e];
+                if (idx < 0 && cum > t && a[e] > 0.0f) idx = e;
+            }
+            if (idx < 0) idx = lastp;
+            mine = (idx >= 0) ? lane * E + idx : -1;
+        }
+        return __builtin_amdgcn_readlane(mine, f);
+    }
+    // t lies at or beyond the sub-chunk total (rounding only): the last positive weight
+    int lastp = -1;
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+        if (a[e] > 0.0f) lastp = lane * E + e;
+    return wave_max_int(lastp);
+}
+
+template <class D, bool kFlat = false, class W>
+__device__ __forceinline__ int wave_sub_chunk_find(const typename D::T* rp, const typename D::T* rq, int n, const W& w,
+                                                   double t) {
+    return (w.kind == kTargetRow) ? wave_sub_chunk_find_k<D, kTargetRow, kFlat>(rp, rq, n, w, t)
+                                  : wave_sub_chunk_find_k<D, kResidual, kFlat>(rp, rq, n, w, t);
+}
+
 // ---------------------------------------------------------------------------
 // the fused step: one launch; a workgroup's role follows from its index
 //   stats (b, s, k)  exact mode: chunk k of stats slot s of batch element b
@@ -1076,6 +1131,72 @@ __device__ __forceinline__ void wave_locate(double m, double u, Smem& sm) {
     }
 }
 
+// mass_prefix + mass_locate by one wave when M <= 4 kWave: lane l holds
+// masses 4 l .. 4 l + 3, as thread l does there, with the same sums, scan and
+// crossing rule, so the same total, mass and remainder, left in
+// sm.cross_tot, sm.cross (-1 if none) and sm.cross_t as wave_locate leaves
+// them; the caller's barrier publishes them.  Called by the lanes of one wave.
+__device__ __forceinline__ void wave_locate4(const double* m, int M, double u, Smem& sm) {
+    const int lane = threadIdx.x % kWave;
+    double loc[4];
+    double ls = 0.0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int k = lane * 4 + i;
+        loc[i] = (k < M) ? m[k] : 0.0;
+        ls += loc[i];
+    }
+    const double incl = wave_inclusive_scan(ls);
+    const double tot = lane_f64(incl, kWave - 1);
+    int j = -1;
+    double tl = 0.0;
+    if (isfinite(tot) && tot > 0.0) {
+        const double t = u * tot;
+        const unsigned long long over = __ballot(incl > t);
+        if (over) {
+            const int f = __ffsll((long long)over) - 1;
+            const double cum0 = (f == 0) ? 0.0 : lane_f64(incl, f - 1);
+            int jl = -1;
+            double rem = 0.0;
+            if (lane == f) {
+                double cum = cum0, before = cum0, lastp_before = 0.0;
+                int lastp = -1;
+                for (int i = 0; i < 4; ++i) {
+                    if (loc[i] > 0.0) {
+                        lastp = lane * 4 + i;
+                        lastp_before = cum;
+                    }
+                    if (jl < 0 && cum + loc[i] > t && loc[i] > 0.0) {
+                        jl = lane * 4 + i;
+                        before = cum;
+                    }
+                    cum += loc[i];
+                }
+                if (jl < 0) {
+                    jl = lastp;
+                    before = lastp_before;
+                }
+                rem = t - before;
+            }
+            j = __builtin_amdgcn_readlane(jl, f);
+            tl = lane_f64(rem, f);
+        } else {
+            // rounding only: the last positive mass, whole
+            int lp = -1;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (loc[i] > 0.0) lp = lane * 4 + i;
+            j = wave_max_int(lp);
+            tl = (j >= 0) ? m[j] : 0.0;
+        }
+    }
+    if (lane == 0) {
+        sm.cross_tot = tot;
+        sm.cross = j;
+        sm.cross_t = tl;
+    }
+}
+
 
 
 // b's decision, made once by b's decider workgroup and, in the exact mode,
@@ -1526,6 +1647,12 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
             total = sm.cross_tot;
             j = sm.cross;
             t_local = sm.cross_t;
+        } else if (kPipe && M <= 4 * kWave) {
+            if (tid < kWave) wave_locate4(sm.sub, M, u, sm);
+            __syncthreads();
+            total = sm.cross_tot;
+            j = sm.cross;
+            t_local = sm.cross_t;
         } else {
             double loc[4];
             total = mass_prefix(sm.sub, M, sm, loc);
@@ -1560,8 +1687,15 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
             break;
         }
         const Span sp = sub_chunk(j / kWaves, j % kWaves, P.chunk2, V, E);
-        const int local = kExact ? sub_chunk_find<D, kPipe>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result)
-                                 : sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result);
+        int local = -1;
+        if (kPipe && kExact && (sp.n + E - 1) / E <= kWave) {
+            // one wave scans (the outputs are thread 0's to write; the other
+            // waves go on to the clears)
+            if (tid < kWave) local = wave_sub_chunk_find<D, kPipe>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, t_local);
+        } else {
+            local = kExact ? sub_chunk_find<D, kPipe>(rp + sp.begin, rq + sp.begin, sp.n, d.ew, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result)
+                           : sub_chunk_find<D>(rp + sp.begin, rq + sp.begin, sp.n, d.sw, t_local, sm.scratch, sm.incl, sm.iscratch, &sm.result);
+        }
         idx = (local >= 0) ? sp.begin + local : -1;
         if (idx < 0) bad = true;
         break;
