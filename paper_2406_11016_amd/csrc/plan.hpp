@@ -27,7 +27,7 @@ constexpr int kMaxGamma = SV_MAX_GAMMA;
 constexpr int kMaxRows = 2 * kMaxGamma + 1;
 constexpr int kUnroll = 8;               // 16-byte loads in flight per thread in the stats stream
 
-constexpr int kWantStatsTiles = 2048;    // enough workgroups to fill 256 CUs several times
+constexpr int kWantStatsTiles = 1024;    // enough workgroups to fill 256 CUs (4 per CU) once
 constexpr int kWantSampleTiles = 1024;
 constexpr int kStatsTileBytes = 32768;   // at most 32 KiB of one row per stats workgroup
 constexpr long long kLagStreamBytes = 56000000;  // stream between an element's stats and its mass tiles
