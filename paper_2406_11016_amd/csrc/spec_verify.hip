@@ -834,6 +834,16 @@ __device__ __forceinline__ double log2_pos(double s) {
     return (double)(e - 1) + (double)__builtin_amdgcn_logf(m) + (M - (double)m) / ((double)m * 0.6931471805599453094);
 }
 
+// log2_pos with the correction term in fp32 (it is below 9e-8, so its fp32
+// rounding is far below the decision margin): no fp64 division on the chain.
+__device__ __forceinline__ double log2_pos_fast(double s) {
+    int e;
+    const double M = 2.0 * frexp(s, &e);  // [1, 2)
+    const float m = (float)M;
+    const float corr = (float)(M - (double)m) * __builtin_amdgcn_rcpf(m) * kLog2e;
+    return (double)(e - 1) + (double)__builtin_amdgcn_logf(m) + (double)corr;
+}
+
 // 2^l for l <= 0 (larger l return 1, the clamp of eq. (1)), to about 1.5e-7
 // relative: 2^floor(l) exactly times the hardware fp32 2^f of the fraction
 // f = l - floor(l) in [0, 1) (its fp32 rounding adds under 3e-8).
@@ -853,6 +863,12 @@ __device__ __forceinline__ double exp2_nonpos(double l) {
 // lane takes the logarithm.  Ends with a workgroup barrier.
 // The group size follows from Rg if given (else R): merging fewer rows with
 // the group size of Rg rows gives each row the same bits as the larger merge.
+// kFast (the short-stream launch, where the merge is on the step's critical
+// chain): a lane's pairs are read from LDS up to four at a time with their
+// loads issued together and kept in registers for the sum, and the logarithm
+// takes log2_pos_fast.  The sums run in the same order, so only the last bits
+// of the logarithm differ from the plain merge.
+template <bool kFast = false>
 __device__ __forceinline__ void merge_rows(Smem& sm, int R, int W, int Rg = 0) {
     const int Rs = (Rg > 0) ? Rg : R;
     const int G = (Rs <= 16) ? 16 : (Rs <= 32) ? 8 : (Rs <= 64) ? 4 : (Rs <= 128) ? 2 : 1;
@@ -863,17 +879,46 @@ __device__ __forceinline__ void merge_rows(Smem& sm, int R, int W, int Rg = 0) {
         const float* K = sm.K + (size_t)i * W;
         const double* S = sm.S + (size_t)i * W;
         float m = -INFINITY;
-        if (row)
-            for (int j = g; j < W; j += G) m = fmaxf(m, K[j]);
-        m = group_max(m, G);
         double sum = 0.0;
-        if (row)
-            for (int j = g; j < W; j += G) sum += ldexp(S[j], exp_delta(K[j] - m));
+        if constexpr (kFast) {
+            constexpr int kBatch = 4;
+            if (W <= kBatch * G) {
+                float kb[kBatch];
+                double sb[kBatch];
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u) {
+                    const int j = g + u * G;
+                    kb[u] = (row && j < W) ? K[j] : -INFINITY;
+                    sb[u] = (row && j < W) ? S[j] : 0.0;
+                }
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u) m = fmaxf(m, kb[u]);
+                m = group_max(m, G);
+#pragma unroll
+                for (int u = 0; u < kBatch; ++u)
+                    if (row && g + u * G < W) sum += ldexp(sb[u], exp_delta(kb[u] - m));
+            } else {
+                if (row)
+                    for (int j = g; j < W; j += G) m = fmaxf(m, K[j]);
+                m = group_max(m, G);
+                if (row)
+                    for (int j = g; j < W; j += G) sum += ldexp(S[j], exp_delta(K[j] - m));
+            }
+        } else {
+            if (row)
+                for (int j = g; j < W; j += G) m = fmaxf(m, K[j]);
+            m = group_max(m, G);
+            if (row)
+                for (int j = g; j < W; j += G) sum += ldexp(S[j], exp_delta(K[j] - m));
+        }
         sum = group_sum(sum, G);
         // a NaN logit makes S NaN; a +inf logit makes K +inf and S NaN
         if (row && g == 0)
             sm.rowL[i] = (sum != sum) ? __builtin_nan("")
-                         : ((m == -INFINITY) ? -INFINITY : (double)m + ((sum > 0.0 && sum < INFINITY) ? log2_pos(sum) : log2(sum)));
+                         : ((m == -INFINITY) ? -INFINITY
+                                             : (double)m + ((sum > 0.0 && sum < INFINITY)
+                                                                ? (kFast ? log2_pos_fast(sum) : log2_pos(sum))
+                                                                : log2(sum)));
     }
     __syncthreads();
 }
@@ -970,7 +1015,7 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
         // max K + log2(sum S 2^(K - max K)) by exact power-of-two scaling
         const int W = P.nchunk1;  // chunks per row
         d.ok = wait_ks<kPipe>(P.pslot + (size_t)b * P.pstride, 2 * gamma * W, sm.K, sm.S, spin_limit(P));
-        merge_rows(sm, 2 * gamma, W);
+        merge_rows<kPipe>(sm, 2 * gamma, W);
     }
 
     int stop = 0;
