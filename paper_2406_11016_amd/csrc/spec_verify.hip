@@ -670,7 +670,10 @@ template <bool kRagged>
 __device__ __forceinline__ int elem_gamma(const StepParams& P, int b, bool* bad) {
     *bad = false;
     if constexpr (!kRagged) return P.gamma;
-    const int g = P.gammas[b];
+    // a scalar load through the constant address space (b is the same in the
+    // whole workgroup and gammas is read-only): after the first workgroup of
+    // a CU it comes from the scalar cache, not through the stream's memory queue
+    const int g = ((const __attribute__((address_space(4))) int32_t*)P.gammas)[b];
     *bad = !(g >= 1 && g <= P.gamma);
     return *bad ? P.gamma : g;
 }
