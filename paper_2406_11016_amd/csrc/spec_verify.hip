@@ -997,18 +997,23 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     const T* draft = static_cast<const T*>(P.draft) + (size_t)b * gamma * V;
     const T* target = static_cast<const T*>(P.target) + (size_t)b * (gamma + 1) * V;
 
-    // independent loads first: tokens, uniforms and the drafted-token logits
+    // independent loads first: tokens, uniforms and the drafted-token logits.
+    // In the short-stream launch with at most kWave drafts every wave takes
+    // all drafts (lane c draft c), so that eq. (1) and the first-rejection
+    // scan need no exchange between waves.
+    const bool inwave = kPipe && gb <= kWave;
+    const int c = inwave ? tid % kWave : tid;
     int x = 0;
     double r = 0.0;
     bool tok_ok = true;
     float zp = 0.0f, zq = 0.0f;
-    if (tid < gb) {
-        x = P.tokens[(size_t)b * gamma + tid];
-        r = (double)P.uniforms[(size_t)b * (gamma + 1) + tid];
+    if (c < gb) {
+        x = P.tokens[(size_t)b * gamma + c];
+        r = (double)P.uniforms[(size_t)b * (gamma + 1) + c];
         tok_ok = (x >= 0 && x < V);
         const int xs = tok_ok ? x : 0;
-        zp = to_f32(target[(size_t)tid * V + xs]);
-        zq = to_f32(draft[(size_t)tid * V + xs]);
+        zp = to_f32(target[(size_t)c * V + xs]);
+        zq = to_f32(draft[(size_t)c * V + xs]);
     }
 
     Decision d{};
@@ -1022,12 +1027,12 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
     }
 
     int stop = 0;
-    if (tid < gb) {
+    if (c < gb) {
         double tau;
         bool row_ok;
         if (kExact) {
-            const double lam_p = sm.rowL[tid];          // target row tid
-            const double lam_q = sm.rowL[gamma + tid];  // draft row tid
+            const double lam_p = sm.rowL[c];          // target row c
+            const double lam_q = sm.rowL[gamma + c];  // draft row c
             row_ok = isfinite(lam_p) && isfinite(lam_q);
             if (zq == -INFINITY) {
                 tau = 1.0;  // q(x) = 0
@@ -1044,13 +1049,22 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
             tau = (qh > 0.0) ? min1(ph / qh) : 1.0;
             row_ok = isfinite(tau);
         }
-        sm.tau[tid] = tau;
+        if (c == tid) sm.tau[c] = tau;
         stop = !row_ok ? 2 : ((r <= tau) ? 0 : 1);
     }
     // the first draft that is rejected (or unreadable) ends the accepted prefix
     int first;
     bool first_bad, tok_bad;
-    scan_stops(stop, tok_ok, sm, &first, &first_bad, &tok_bad);
+    if (inwave) {
+        const unsigned long long rej = __ballot(stop != 0);
+        const unsigned long long unr = __ballot(stop == 2);
+        const int l = rej ? __ffsll((long long)rej) - 1 : 0;
+        first = rej ? l : kThreads;
+        first_bad = rej && ((unr >> l) & 1ull) != 0;
+        tok_bad = __ballot(!tok_ok) != 0ull;
+    } else {
+        scan_stops(stop, tok_ok, sm, &first, &first_bad, &tok_bad);
+    }
     d.L = min(first, gb);
     d.gb = gb;
     // target row gb is the bonus role's business (it sentinels a non-finite
