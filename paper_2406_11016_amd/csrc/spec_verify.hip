@@ -1303,15 +1303,58 @@ __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& s
     }
 }
 
+// The decision held in a record's five words (rec, as published), with ok
+// false when the wait for them timed out.
+__device__ __forceinline__ Decision decode_record(const StepParams& P, const unsigned long long* rec, bool ok,
+                                                  bool exact);
+
 // Copy `copy` of b's published decision (in b's mass, draw and bonus
 // workgroups), cleared once read.
 template <bool kPipe = false>
 __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, int copy, bool exact, Smem& sm) {
-    Decision d{};
     unsigned long long* src = P.dslot + ((size_t)b * P.ncopy + copy) * kDecisionWords;
-    d.ok = wait_raw<kPipe>(src, kDecisionWords, sm.rec, spin_limit(P));
+    const bool ok = wait_raw<kPipe>(src, kDecisionWords, sm.rec, spin_limit(P));
     if ((int)threadIdx.x < kDecisionWords) clear_word(src + threadIdx.x);
-    const unsigned long long w0 = sm.rec[0];
+    return decode_record(P, sm.rec, ok, exact);
+}
+
+// The record's words (raw, as published) by one wave on its own: lanes
+// 0 .. 4 poll them with two polls in flight and the wave goes on as soon as
+// it has all five, with no exchange with the other waves of its workgroup
+// (which poll their own).  rec receives the words in every lane.  The caller
+// clears the record once every wave has read it.
+__device__ __forceinline__ bool wave_wait_record(const unsigned long long* src, unsigned long long* rec, int limit) {
+    const int lane = threadIdx.x % kWave;
+    const unsigned long long* p = src + min(lane, kDecisionWords - 1);
+    const bool mine = lane < kDecisionWords;
+    unsigned long long a = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), c = 0ull, w = 0ull;
+    bool ok = false;
+    for (int round = 0;; round += 2) {
+        c = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (__ballot(mine && a == 0ull) == 0ull) {
+            w = a;
+            ok = true;
+            break;
+        }
+        if (round + 1 >= limit) break;
+        a = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (__ballot(mine && c == 0ull) == 0ull) {
+            w = c;
+            ok = true;
+            break;
+        }
+        if (round + 2 >= limit) break;
+    }
+#pragma unroll
+    for (int k = 0; k < kDecisionWords; ++k) rec[k] = ~lane_u64(w, k);
+    return ok;
+}
+
+__device__ __forceinline__ Decision decode_record(const StepParams& P, const unsigned long long* rec, bool ok,
+                                                  bool exact) {
+    Decision d{};
+    d.ok = ok;
+    const unsigned long long w0 = rec[0];
     d.L = d.ok ? (int)(w0 & 0xffff) : 0;
     d.gb = d.ok ? (int)((w0 >> 40) & 0xffff) : P.gamma;
     d.bad = ((w0 >> 16) & 1) != 0 || !d.ok;
@@ -1327,14 +1370,14 @@ __device__ __forceinline__ Decision read_decision(const StepParams& P, int b, in
     if (exact) {
         d.ew.kind = kind;
         d.ew.c = P.c;
-        d.ew.kp = unpack_hi(sm.rec[1]);
-        d.ew.lp_hi = unpack_lo(sm.rec[1]);
-        d.ew.lp_lo = unpack_hi(sm.rec[2]);
-        d.ew.kq = unpack_lo(sm.rec[2]);
-        d.ew.lq_hi = unpack_hi(sm.rec[3]);
-        d.ew.lq_lo = unpack_lo(sm.rec[3]);
-        d.ew.d_hi = unpack_hi(sm.rec[4]);
-        d.ew.d_lo = unpack_lo(sm.rec[4]);
+        d.ew.kp = unpack_hi(rec[1]);
+        d.ew.lp_hi = unpack_lo(rec[1]);
+        d.ew.lp_lo = unpack_hi(rec[2]);
+        d.ew.kq = unpack_lo(rec[2]);
+        d.ew.lq_hi = unpack_hi(rec[3]);
+        d.ew.lq_lo = unpack_lo(rec[3]);
+        d.ew.d_hi = unpack_hi(rec[4]);
+        d.ew.d_lo = unpack_lo(rec[4]);
     } else {
         d.sw.kind = kind;
         d.sw.s = P.s;
@@ -1654,22 +1697,39 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
     constexpr int E = D::E;
     const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-    const Decision d = decision_of<D, kExact, kRagged, kPipe>(P, b, k2, sm);
-    if (!d.ok && tid == 0) set_error(P);
+    // short streams: each wave waits for the decision on its own (the record
+    // is cleared at the end, once every wave has read it)
+    constexpr bool kOwn = kPipe && kExact;
+    unsigned long long* src = P.dslot + ((size_t)b * P.ncopy + k2) * kDecisionWords;
+    Decision d;
+    if constexpr (kOwn) {
+        unsigned long long rec[kDecisionWords];
+        const bool ok = wave_wait_record(src, rec, spin_limit(P));
+        d = decode_record(P, rec, ok, true);
+        if (!d.ok && lane == 0) set_error(P);
+    } else {
+        d = decision_of<D, kExact, kRagged, kPipe>(P, b, k2, sm);
+        if (!d.ok && tid == 0) set_error(P);
+    }
     // b's bonus workgroup draws when every draft is accepted: nothing to do here
     const bool drawn = !d.bad && d.L == d.gb;
-    if (drawn) return;
-    const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
-    double m = 0.0;
-    if (!d.ok) {
-        m = __builtin_nan("");
-    } else if (!d.bad && sp.n > 0) {
-        const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V + sp.begin;
-        const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V + sp.begin;
-        float* wout = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V + sp.begin : nullptr;
-        m = kExact ? wave_weight_sum<D, kPipe>(rp, rq, sp.n, d.ew, wout) : wave_weight_sum<D>(rp, rq, sp.n, d.sw, wout);
+    if (!drawn) {
+        const Span sp = sub_chunk(k2, wave, P.chunk2, V, E);
+        double m = 0.0;
+        if (!d.ok) {
+            m = __builtin_nan("");
+        } else if (!d.bad && sp.n > 0) {
+            const T* rp = static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V + sp.begin;
+            const T* rq = static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V + sp.begin;
+            float* wout = (P.weight_out != nullptr) ? P.weight_out + (size_t)b * V + sp.begin : nullptr;
+            m = kExact ? wave_weight_sum<D, kPipe>(rp, rq, sp.n, d.ew, wout) : wave_weight_sum<D>(rp, rq, sp.n, d.sw, wout);
+        }
+        if (lane == 0) publish(P.mslot + ((size_t)b * P.nchunk2 + k2) * kWaves + wave, m);
     }
-    if (lane == 0) publish(P.mslot + ((size_t)b * P.nchunk2 + k2) * kWaves + wave, m);
+    if constexpr (kOwn) {
+        __syncthreads();
+        if (tid < kDecisionWords) clear_word(src + tid);
+    }
 }
 
 // The inverse-CDF draw for b, by b's draw workgroup, once b's mass tiles have
