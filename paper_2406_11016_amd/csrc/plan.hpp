@@ -30,6 +30,7 @@ constexpr int kUnroll = 8;               // 16-byte loads in flight per thread i
 constexpr int kWantStatsTiles = 1024;    // enough workgroups to fill 256 CUs (4 per CU) once
 constexpr int kWantSampleTiles = 1024;
 constexpr int kStatsTileBytes = 32768;   // at most 32 KiB of one row per stats workgroup
+constexpr long long kSelfDecideWords = 16384;     // pair copies polled by self-deciding mass workgroups
 constexpr long long kLagStreamBytes = 56000000;  // stream between an element's stats and its mass tiles
 constexpr int kGammaTileBytes = 16384;   // target rows gamma, streamed last: short tiles end the stream sharply
 constexpr int kSampleTileBytes = 32768;
@@ -84,11 +85,14 @@ struct Plan {
     int chunk2, nchunk2;     // final-distribution tiles
     int chunkg, nchunkg;     // target row gamma: short tiles, one (K, S) pair per quarter
     long long pstride;       // stats words per batch element
+    long long qstride;       // words of one mass workgroup's copy of the decision rows' pairs (0: no copies)
     long long n_stats, n_mass;
     int gwords;              // row-staged early exit: gate words per stage
     long long gstride;       //                        and gate + state words per batch element
-    size_t off_dslot, off_pslot, off_mslot, off_gslot, bytes;
+    size_t off_dslot, off_pslot, off_mslot, off_gslot, off_qslot, bytes;
 };
+
+inline bool pipelined_waits(long long B, long long gamma, long long V, sv_dtype_t dt);
 
 inline bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* p) {
     if (B < 1 || gamma < 1 || gamma > kMaxGamma || V < 1 || !valid_dtype(dt)) return false;
@@ -153,6 +157,13 @@ inline bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     p->gstride = (long long)(gamma + 1) * p->gwords + gamma;
     p->off_gslot = off;
     off = align256(off + sizeof(unsigned long long) * (size_t)B * p->gstride);
+    // short streams with few pairs to copy: each mass workgroup decides for
+    // itself from its own copy of the decision rows' (K, S) pairs
+    p->qstride = (pipelined_waits(B, gamma, V, dt) && (long long)B * p->nchunk2 * 2 * R * p->nchunk1 <= kSelfDecideWords)
+                     ? 2 * R * p->nchunk1
+                     : 0;
+    p->off_qslot = off;
+    off = align256(off + sizeof(unsigned long long) * (size_t)B * p->nchunk2 * p->qstride);
     p->bytes = off;
     return true;
 }

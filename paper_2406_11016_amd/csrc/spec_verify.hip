@@ -606,6 +606,8 @@ struct StepParams {
     float s, s0;                   // sigmoid: u = fma(z, s, s0)
     int ncopy;                     // copies of each decision record (one per reader)
     int pstride;                   // stats words per batch element
+    unsigned long long* qslot;     // short streams: [B, nchunk2, qstride] the mass workgroups' copies of the pairs
+    int qstride;
     const int32_t* tokens;
     const float* uniforms;
     const int32_t* gammas;         // ragged variant: drafts of each batch element (1 .. gamma)
@@ -692,8 +694,9 @@ __device__ __forceinline__ void split3(double v, float& hi, float& mid, float& l
 // S 2^K, merged later by exact power-of-two scaling.  Wave w streams the
 // contiguous quarter sub_chunk(k, w, ...) of the chunk; the quarters merge
 // in wave order.
-template <class D, bool kRagged>
+template <class D, bool kRagged, bool kPipe = false>
 __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot, int k, Smem& sm) {
+    static_assert(!(kPipe && kRagged), "the short-stream launch is not ragged");
     using T = typename D::T;
     constexpr int E = D::E;
     const int gamma = P.gamma, V = P.V;
@@ -763,6 +766,20 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot,
                 P.pslot + (size_t)b * P.pstride + ((size_t)slot * P.nchunk1 + (size_t)k * kWaves + wave) * 2;
             publish(out, (double)w.k);
             publish(out + 1, w.s);
+        }
+        return;
+    }
+    if constexpr (kPipe) {
+        // short streams: the pair goes to b's decider and to each of b's mass
+        // workgroups (which decide for themselves), one copy per thread
+        const Lse t = block_lse_all(st, sm.sk, sm.ss);
+        const size_t at = ((size_t)slot * P.nchunk1 + k) * 2;
+        const int ncp = (P.qstride > 0) ? P.nchunk2 : 0;
+        for (int j = threadIdx.x; j <= ncp; j += kThreads) {
+            unsigned long long* out = (j == 0) ? P.pslot + (size_t)b * P.pstride + at
+                                               : P.qslot + ((size_t)b * P.nchunk2 + (j - 1)) * P.qstride + at;
+            publish(out, (double)t.k);
+            publish(out + 1, t.s);
         }
         return;
     }
@@ -988,7 +1005,7 @@ struct Decision {
 // The decision for batch element b: eq. (1) at the drafted tokens and the
 // first-rejection scan, plus the weights of the final distribution.
 template <class D, bool kExact, bool kRagged, bool kPipe = false>
-__device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm) {
+__device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm, unsigned long long* ks = nullptr) {
     using T = typename D::T;
     const int gamma = P.gamma, V = P.V;
     const int tid = threadIdx.x;
@@ -1022,7 +1039,8 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm)
         // the stats slots the decision reads, merged into log2-normalisers
         // max K + log2(sum S 2^(K - max K)) by exact power-of-two scaling
         const int W = P.nchunk1;  // chunks per row
-        d.ok = wait_ks<kPipe>(P.pslot + (size_t)b * P.pstride, 2 * gamma * W, sm.K, sm.S, spin_limit(P));
+        d.ok = wait_ks<kPipe>((ks != nullptr) ? ks : P.pslot + (size_t)b * P.pstride, 2 * gamma * W, sm.K, sm.S,
+                              spin_limit(P));
         merge_rows<kPipe>(sm, 2 * gamma, W);
     }
 
@@ -1268,14 +1286,14 @@ __device__ __forceinline__ void wave_locate4(const double* m, int M, double u, S
 // words it read (it is their only reader).
 // The P.ncopy copies of b's decision record (L, the sentinel flag, gb and the
 // residual's constants), written by every thread of the workgroup.
-__device__ __forceinline__ void publish_decision(const StepParams& P, int b, const Decision& d) {
+__device__ __forceinline__ void publish_decision(const StepParams& P, int b, const Decision& d, int first = 0) {
     const unsigned long long rec[kDecisionWords] = {
         (unsigned long long)(d.L & 0xffff) | ((unsigned long long)(d.bad ? 1 : 0) << 16) | (1ull << 32) |
             ((unsigned long long)(d.gb & 0xffff) << 40),
         pack2(d.ew.kp, d.ew.lp_hi), pack2(d.ew.lp_lo, d.ew.kq), pack2(d.ew.lq_hi, d.ew.lq_lo),
         pack2(d.ew.d_hi, d.ew.d_lo)};
     unsigned long long* dst = P.dslot + (size_t)b * P.ncopy * kDecisionWords;
-    for (int i = threadIdx.x; i < P.ncopy * kDecisionWords; i += kThreads) {
+    for (int i = first * kDecisionWords + (int)threadIdx.x; i < P.ncopy * kDecisionWords; i += kThreads) {
         const int w = i % kDecisionWords;
         unsigned long long v = rec[0];
 #pragma unroll
@@ -1290,9 +1308,10 @@ __device__ __forceinline__ void decider_role(const StepParams& P, int b, Smem& s
     const int tid = threadIdx.x;
     const Decision d = decide<D, kExact, kRagged, kPipe>(P, b, sm);
     if (!d.ok && tid == 0) set_error(P);
-    // (sigmoid mode: the mass and draw workgroups decide for themselves, so
-    // the only copy, if any, is the bonus workgroup's)
-    publish_decision(P, b, d);
+    // (sigmoid mode and the short streams' mass workgroups decide for
+    // themselves: the sigmoid mode's only copy is the bonus workgroup's, the
+    // short streams' are the draw's and the bonus workgroup's)
+    publish_decision(P, b, d, (kPipe && kExact && P.qstride > 0) ? P.nchunk2 : 0);
     if (P.tau_out != nullptr && tid < gamma) P.tau_out[(size_t)b * gamma + tid] = sm.tau[tid];
     if (kExact) {
         const int W = P.nchunk1;
@@ -1691,6 +1710,29 @@ __device__ __forceinline__ Decision decision_of(const StepParams& P, int b, int 
     return decide<D, false, kRagged>(P, b, sm);
 }
 
+// Touches one element in each 128-byte line of rows p and q, elements
+// [0, n) each (lines j0, j0 + stride, ...; up to 8 per row in flight), so
+// that later loads of them hit the L2 of this workgroup's XCD.  Waits for
+// the loads.
+template <class T>
+__device__ __forceinline__ void touch_rows(const T* p, const T* q, int n, int j0, int stride) {
+    constexpr int kStep = 128 / (int)sizeof(T);
+    const int nl = (n + kStep - 1) / kStep;
+    float t = 0.0f;
+    for (int l0 = j0; l0 < nl; l0 += 8 * stride) {
+        float a[8], c[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = min((l0 + u * stride) * kStep, n - 1);
+            a[u] = to_f32(p[i]);
+            c[u] = to_f32(q[i]);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) t += a[u] + c[u];
+    }
+    asm volatile("" ::"v"(t));
+}
+
 template <class D, bool kExact, bool kRagged, bool kPipe = false>
 __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Smem& sm) {
     using T = typename D::T;
@@ -1700,9 +1742,13 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
     // short streams: each wave waits for the decision on its own (the record
     // is cleared at the end, once every wave has read it)
     constexpr bool kOwn = kPipe && kExact;
-    unsigned long long* src = P.dslot + ((size_t)b * P.ncopy + k2) * kDecisionWords;
+    unsigned long long* ks = P.qslot + ((size_t)b * P.nchunk2 + k2) * P.qstride;
     Decision d;
-    if constexpr (kOwn) {
+    unsigned long long* src = P.dslot + ((size_t)b * P.ncopy + k2) * kDecisionWords;
+    if (kOwn && P.qstride > 0) {
+        d = decide<D, true, kRagged, true>(P, b, sm, ks);
+        if (!d.ok && tid == 0) set_error(P);
+    } else if (kOwn) {
         unsigned long long rec[kDecisionWords];
         const bool ok = wave_wait_record(src, rec, spin_limit(P));
         d = decode_record(P, rec, ok, true);
@@ -1726,7 +1772,9 @@ __device__ __forceinline__ void mass_role(const StepParams& P, int b, int k2, Sm
         }
         if (lane == 0) publish(P.mslot + ((size_t)b * P.nchunk2 + k2) * kWaves + wave, m);
     }
-    if constexpr (kOwn) {
+    if (kOwn && P.qstride > 0) {
+        for (int i = tid; i < P.qstride; i += kThreads) clear_word(ks + i);
+    } else if (kOwn) {
         __syncthreads();
         if (tid < kDecisionWords) clear_word(src + tid);
     }
@@ -1748,6 +1796,9 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
     const bool drawn = !d.bad && d.L == d.gb;
     if (!d.ok && tid == 0) set_error(P);
     if (drawn) return;
+    if (kPipe && kExact && 2LL * V * (long long)sizeof(T) <= (128ll << 10))
+        touch_rows(static_cast<const T*>(P.target) + ((size_t)b * (gamma + 1) + min(d.L, gamma)) * V,
+                   static_cast<const T*>(P.draft) + ((size_t)b * gamma + min(d.L, gamma - 1)) * V, V, tid, kThreads);
     unsigned long long* ms = P.mslot + (size_t)b * M;
     const bool got = d.ok && wait_words<kPipe>(ms, M, sm.sub, spin_limit(P));
     if (d.ok && !got && tid == 0) set_error(P);
@@ -2046,7 +2097,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     const unsigned int S = (unsigned int)Y.S;
     if (r < S) {
         const int slot = (int)div_of(Y.dc1, r);
-        stats_role<D, kRagged>(P, bs, slot, (int)r - slot * P.nchunk1, sm);
+        stats_role<D, kRagged, kPipe>(P, bs, slot, (int)r - slot * P.nchunk1, sm);
         return;
     }
     if (r == S) {
@@ -2132,6 +2183,8 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
     P.nchunkg = pl.nchunkg;
     P.ncopy = decision_copies(exact, pl);
     P.pstride = (int)pl.pstride;
+    P.qstride = (int)pl.qstride;
+    P.qslot = reinterpret_cast<unsigned long long*>(ws + pl.off_qslot);
     P.y = single_pass_layout(a.B, a.gamma, a.V, a.dt, exact, pl);
     const long long n_total = (long long)P.y.end2 + a.B;
     P.temperature = (double)a.temperature;

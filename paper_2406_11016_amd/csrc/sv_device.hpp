@@ -336,4 +336,20 @@ __device__ __forceinline__ Lse block_lse(Lse st, float* sk /* [kWaves] */, doubl
     return out;
 }
 
+// block_lse with the result in every thread (same bits as block_lse's thread 0).
+__device__ __forceinline__ Lse block_lse_all(Lse st, float* sk /* [kWaves] */, double* ss /* [kWaves] */) {
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    const Lse w = wave_lse(st);
+    if (lane == 0) {
+        sk[wave] = w.k;
+        ss[wave] = w.s;
+    }
+    __syncthreads();
+    Lse out{sk[0], ss[0]};
+#pragma unroll
+    for (int i = 1; i < kWaves; ++i) out = lse_merge(out, Lse{sk[i], ss[i]});
+    return out;
+}
+
 }  // namespace sv

@@ -99,10 +99,16 @@ static void check_plan(int B, int gamma, int V, sv_dtype_t dt, const Plan& p) {
     CHECK(p.pstride == 2 * (2LL * gamma * p.nchunk1 + (long long)kWaves * p.nchunkg), "pstride");
     CHECK(p.off_mslot >= p.off_pslot + w * (size_t)B * (size_t)p.pstride, "pslot size");
     CHECK(p.off_gslot >= p.off_mslot + w * (size_t)B * p.nchunk2 * kWaves, "mslot size");
-    CHECK(p.bytes >= p.off_gslot + w * (size_t)B * (size_t)p.gstride, "gslot size");
+    CHECK(p.off_qslot % 256 == 0 && p.off_qslot >= p.off_gslot + w * (size_t)B * (size_t)p.gstride, "gslot size");
+    // the self-deciding mass workgroups' pair copies: only for short streams
+    // with few words to copy, one copy of every decision-row pair per tile
+    CHECK(p.qstride == 0 || (pipelined_waits(B, gamma, V, dt) && p.qstride == 4LL * gamma * p.nchunk1 &&
+                             (long long)B * p.nchunk2 * p.qstride <= kSelfDecideWords),
+          "qstride %lld", p.qstride);
+    CHECK(p.bytes >= p.off_qslot + w * (size_t)B * p.nchunk2 * (size_t)p.qstride, "qslot size");
     CHECK(p.gwords >= 2 * p.nchunk1 && p.gwords >= p.nchunkg, "gwords");
     // the kernels index the stats words with int
-    CHECK(p.pstride < 0x7fffffffLL && p.gstride < 0x7fffffffLL, "strides");
+    CHECK(p.pstride < 0x7fffffffLL && p.gstride < 0x7fffffffLL && p.qstride < 0x7fffffffLL, "strides");
 }
 
 static std::vector<int> batch_grid() { return {1, 2, 3, 5, 7, 16, 17, 32, 63, 64, 65, 128, 257, 1000, 4096}; }
