@@ -364,6 +364,15 @@ static void section_pipelined_waits() {
         for (long long g : {1LL, 8LL, 128LL})
             for (long long V : {1LL, 4097LL, 1LL << 20})
                 CHECK(pipelined_waits(B, g, V, SV_F32) == (2 * g * V * 4 * B < kLagStreamBytes), "rule");
+    // which short streams' mass workgroups decide for themselves (pair
+    // copies): the named B = 1 fp16 workload and the reduced test shapes do,
+    // the named B = 1 and B = 16 fp32 workloads wait for the decider's record
+    Plan p{};
+    CHECK(make_plan(1, 10, 32000, SV_F16, &p) && p.qstride == 4LL * 10 * p.nchunk1, "B=1 fp16 copies");
+    CHECK(make_plan(1, 5, 9001, SV_F32, &p) && p.qstride > 0, "reduced B=1 fp32 copies");
+    CHECK(make_plan(1, 5, 51865, SV_F32, &p) && p.qstride == 0, "B=1 fp32 record");
+    CHECK(make_plan(16, 5, 51865, SV_F32, &p) && p.qstride == 0, "B=16 fp32 record");
+    CHECK(make_plan(64, 8, 128256, SV_BF16, &p) && p.qstride == 0, "long stream: no copies");
     printf("pipelined waits: ok\n");
 }
 
