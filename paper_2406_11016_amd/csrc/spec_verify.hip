@@ -688,6 +688,30 @@ __device__ __forceinline__ void split3(double v, float& hi, float& mid, float& l
     lo = (float)((v - (double)hi) - (double)mid);
 }
 
+// The lane's whole vectors l, l + 64, ... of a chunk of nfull vectors at
+// base, absorbed in blocks of U (all loads of a block issued before any is
+// used, the block sharing one update of the running reference).
+template <int U, class D>
+__device__ __forceinline__ void stats_stream(const typename D::T* base, int nfull, bool aligned, int lane, float c,
+                                             Lse& st) {
+    constexpr int E = D::E;
+    for (int v0 = 0; v0 < nfull; v0 += U * kWave) {
+        float x[U][E];
+        if (aligned) {
+            u32x4 raw[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) raw[u] = load_vec_or_pad<D, true>(base, v0 + u * kWave + lane, nfull);
+#pragma unroll
+            for (int u = 0; u < U; ++u) unpack<D>(raw[u], x[u]);
+        } else {
+            // rows that are not 4-byte aligned (16-bit logits with odd V)
+#pragma unroll
+            for (int u = 0; u < U; ++u) load_elems_or_pad<D>(base, (v0 + u * kWave + lane) * E, nfull * E, x[u]);
+        }
+        lse_absorb_block<U, E>(st, x, c);
+    }
+}
+
 // Exact mode, one chunk of one row: sum_x 2^(z c - K) in one streaming pass,
 // published as the pair (K, S): K an integral reference (or -inf), S the fp64
 // sum of 2^(z c - K) over the chunk, so sum_x e^(z/T) = sum over chunks of
@@ -736,21 +760,35 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot,
     // depend only on element indices, never on the row's address, so equal
     // rows give bit-identical sums.
     Lse st{-INFINITY, 0.0};
-    for (int v0 = 0; v0 < nfull; v0 += kUnroll * kWave) {
-        float x[kUnroll][E];
-        if (aligned) {
-            u32x4 raw[kUnroll];
+    if constexpr (kPipe) {
+        // short streams: blocks no deeper than the lane's vectors (short
+        // chunks hold one or two per lane)
+        const int per_lane = (nfull + kWave - 1) / kWave;
+        if (per_lane <= 1)
+            stats_stream<1, D>(base, nfull, aligned, lane, c, st);
+        else if (per_lane <= 2)
+            stats_stream<2, D>(base, nfull, aligned, lane, c, st);
+        else if (per_lane <= 4)
+            stats_stream<4, D>(base, nfull, aligned, lane, c, st);
+        else
+            stats_stream<kUnroll, D>(base, nfull, aligned, lane, c, st);
+    } else {
+        for (int v0 = 0; v0 < nfull; v0 += kUnroll * kWave) {
+            float x[kUnroll][E];
+            if (aligned) {
+                u32x4 raw[kUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) raw[u] = load_vec_or_pad<D, true>(base, v0 + u * kWave + lane, nfull);
+                for (int u = 0; u < kUnroll; ++u) raw[u] = load_vec_or_pad<D, true>(base, v0 + u * kWave + lane, nfull);
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) unpack<D>(raw[u], x[u]);
-        } else {
-            // rows that are not 4-byte aligned (16-bit logits with odd V)
+                for (int u = 0; u < kUnroll; ++u) unpack<D>(raw[u], x[u]);
+            } else {
+                // rows that are not 4-byte aligned (16-bit logits with odd V)
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-                load_elems_or_pad<D>(base, (v0 + u * kWave + lane) * E, nfull * E, x[u]);
+                for (int u = 0; u < kUnroll; ++u)
+                    load_elems_or_pad<D>(base, (v0 + u * kWave + lane) * E, nfull * E, x[u]);
+            }
+            lse_absorb_block<kUnroll, E>(st, x, c);
         }
-        lse_absorb_block<kUnroll, E>(st, x, c);
     }
     if (n > nfull * E && lane == nfull % kWave) {
         float x[1][E];
@@ -1430,24 +1468,20 @@ __device__ __forceinline__ int wave_find_target(const typename D::T* rp, int n, 
     const unsigned long long over = __ballot(incl > t);
     int mine = -1;
     if (over) {
+        // the crossing lane f's NE elements, one per lane (lanes below NE
+        // read element f NE + lane again, now from cache), weighed and
+        // scanned across the wave on top of the mass before lane f
+        static_assert(NE <= kWave, "one element per lane");
         const int f = __ffsll((long long)over) - 1;
         const double before = (f == 0) ? 0.0 : lane_f64(incl, f - 1);
-        if (lane == f) {
-            double cum = before;
-            int idx = -1, lastp = -1;
-#pragma unroll
-            for (int v = 0; v < NV; ++v)
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const float a = w.template eval<kTargetRow>(z[v][e], -INFINITY);
-                    if (a > 0.0f) lastp = v * E + e;
-                    cum += (double)a;
-                    if (idx < 0 && cum > t && a > 0.0f) idx = v * E + e;
-                }
-            if (idx < 0) idx = lastp;
-            mine = (idx >= 0) ? lane * NE + idx : -1;
-        }
-        return __builtin_amdgcn_readlane(mine, f);
+        const int i = f * NE + lane;
+        const bool mine_el = lane < NE && i < n;
+        const float a = mine_el ? w.template eval<kTargetRow>(to_f32(rp[max(min(i, n - 1), 0)]), -INFINITY) : 0.0f;
+        const double cum = before + wave_inclusive_scan((double)a);
+        const unsigned long long hit = __ballot(mine_el && cum > t && a > 0.0f);
+        const unsigned long long pos = __ballot(mine_el && a > 0.0f);
+        const int idx = hit ? __ffsll((long long)hit) - 1 : (pos ? 63 - __clzll((long long)pos) : -1);
+        return (idx >= 0) ? f * NE + idx : -1;
     }
     // t lies at or beyond the total (rounding only): the last positive weight
 #pragma unroll
