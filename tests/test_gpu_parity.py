@@ -83,6 +83,18 @@ def test_gamma_range(gamma):
         _report(f"gamma={gamma}", x, nflag)
 
 
+@pytest.mark.parametrize("B,gamma,V,dtype", [(2, 3, 65537, "f16"), (8, 8, 20011, "bf16"), (16, 2, 40000, "f32"),
+                                              (16, 4, 40000, "f32")])
+def test_short_stream_block_depths(B, gamma, V, dtype):
+    # short streams whose stats chunks hold 1, 2, 4 and 8 vectors per lane
+    # (the stats blocks take that depth); mixed acceptance, so the residual
+    # and the bonus draws both run
+    for noise in (0.2, 1.0):
+        x = W.small_case(B, gamma, V, dtype, seed=300 + B + gamma, noise_scale=noise)
+        nflag = compare(x, run_gpu(x), run_oracle(x), label=f"depths B={B} g={gamma} V={V} {dtype} noise={noise}")
+        _report(f"block depths noise={noise}", x, nflag)
+
+
 @pytest.mark.parametrize("mode", ["exact", "sigmoid"])
 def test_unaligned_rows_and_offsets(mode):
     # odd V in fp32: every row after the first starts off a 16-byte boundary;
