@@ -167,9 +167,12 @@ sv_status_t spec_verify_exact(const void* draft_logits, const void* target_logit
                               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
- * Exact mode with an early exit: the same result as spec_verify_exact
- * (bit-identical outputs), computed so that the logit rows a batch element
- * does not need are mostly not read.  Sec. 3.1 stops the acceptance scan at
+ * Exact mode with an early exit: the same result as spec_verify_exact,
+ * computed so that the logit rows a batch element does not need are mostly
+ * not read.  Its row chunks are twice as long as spec_verify_exact's, so its
+ * row normalisers can differ from that call's in the last bits: a decision
+ * can differ only where a uniform lies within that rounding of its
+ * threshold.  Sec. 3.1 stops the acceptance scan at
  * the first rejection L, so the rows of positions after L (and target row
  * gamma when L < gamma) play no part in the result.  The rows stream in draft
  * order (stage c: target row c and draft row c of every batch element), each

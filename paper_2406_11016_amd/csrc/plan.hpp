@@ -82,6 +82,7 @@ inline Div make_div(unsigned int d) {
 struct Plan {
     int E;                   // elements per 16-byte vector
     int chunk1, nchunk1;     // decision rows: chunk length and chunks per row
+    int chunk1s, nchunk1s;   // the same for the row-staged early exit (twice as long)
     int chunk2, nchunk2;     // final-distribution tiles
     int chunkg, nchunkg;     // target row gamma: short tiles, one (K, S) pair per quarter
     long long pstride;       // stats words per batch element
@@ -116,6 +117,12 @@ inline bool make_plan(int32_t B, int32_t gamma, int32_t V, sv_dtype_t dt, Plan* 
     p->chunk1 = (int)chunk;
     p->nchunk1 = (int)ceil_div(V, chunk);
     if (R1 * p->nchunk1 > kMaxStatsSub) return false;
+    // the row-staged early exit streams chunks twice as long: when most of
+    // its rows are skipped it is bound by how fast workgroups are dispatched,
+    // not by HBM, so fewer of them pay
+    const long long chunks = ceil_div(ceil_div(V, std::max(1LL, ceil_div(p->nchunk1, 2))), E) * E;
+    p->chunk1s = (int)chunks;
+    p->nchunk1s = (int)ceil_div(V, chunks);
 
     // target row gamma in short tiles whose quarters fit the bonus draw's scan
     // (at most one vector per thread of a workgroup); the row's quarter masses
@@ -391,7 +398,7 @@ inline int gate_stages(long long B, long long V, long long s) {
 // Workgroups of the staged launch, or -1 when the staged order cannot skip
 // any row (gate >= gamma: the single pass serves) or exceeds 2^31 workgroups.
 inline long long staged_workgroups(long long B, long long gamma, long long V, sv_dtype_t dt, const Plan& pl) {
-    const long long n = B * (gamma * (2LL * pl.nchunk1 + 1) + 1 + pl.nchunkg + pl.nchunk2 + 2);
+    const long long n = B * (gamma * (2LL * pl.nchunk1s + 1) + 1 + pl.nchunkg + pl.nchunk2 + 2);
     if (gate_stages(B, V, bytes_per_logit(dt)) >= gamma || n > 0x7fffffffLL) return -1;
     return n;
 }
@@ -399,8 +406,8 @@ inline long long staged_workgroups(long long B, long long gamma, long long V, sv
 // The decoding loop's automatic choice of the early exit for the next step:
 // after a step of `gamma` drafts whose accepted lengths sum to `accepted_sum`
 // over B elements, the early exit pays when the mean accepted length is below
-// gamma / 2 (it measured 1.24-1.48x the single pass at mean accepted 1.23 ..
-// 0.02 of gamma 8, and 0.78x at 7.41).
+// gamma / 2 (it measured 1.16-1.59x the single pass at mean accepted 1.23 ..
+// 0.02 of gamma 8, and 0.77x at 7.41).
 inline bool early_exit_pays(long long accepted_sum, long long B, int gamma) {
     return B > 0 && 2 * accepted_sum < (long long)gamma * B;
 }

@@ -1934,8 +1934,10 @@ __device__ __forceinline__ void draw_role(const StepParams& P, int b, Smem& sm) 
 // without settling b hands "running" to row decider c + 1 and "stream" to
 // the tiles of stage c + gate.  Every word still has one writer and one
 // reader, which clears it.  The merges, eq. (1) and the record are those of
-// the single-pass decider, so the outputs are bit-identical to
-// verify_kernel's.
+// the single-pass decider; the decision rows stream in chunks twice as long
+// as verify_kernel's (fewer workgroups to dispatch when most rows are
+// skipped), so the normalisers, and with them the outputs, can differ from
+// verify_kernel's only by rounding in the last bits.
 // ---------------------------------------------------------------------------
 enum : unsigned long long { kStateRunning = 1, kStateSettled = 2, kGateStream = 1, kGateSkip = 2 };
 
@@ -2247,7 +2249,9 @@ static sv_status_t launch(const Call& a, bool exact, const Plan& pl) {
         P.gwords = pl.gwords;
         P.gstride = (int)pl.gstride;
         P.gate = gate_stages(a.B, a.V, bytes_per_logit(a.dt));
-        P.y = make_staged_layout(a.B, a.gamma, pl.nchunk1, pl.nchunkg, pl.nchunk2);
+        P.chunk1 = pl.chunk1s;
+        P.nchunk1 = pl.nchunk1s;
+        P.y = make_staged_layout(a.B, a.gamma, pl.nchunk1s, pl.nchunkg, pl.nchunk2);
         const dim3 sgrid((unsigned int)((long long)P.y.end2 + a.B)), sblock(kThreads);
         hipLaunchKernelGGL((staged_kernel<D>), sgrid, sblock, 0, a.stream, P);
         return hipGetLastError() == hipSuccess ? SV_OK : SV_ERR_HIP;

@@ -78,6 +78,12 @@ static void check_plan(int B, int gamma, int V, sv_dtype_t dt, const Plan& p) {
     CHECK(p.chunk1 % E == 0 && p.chunk1 > 0, "chunk1 %d", p.chunk1);
     CHECK((long long)p.nchunk1 * p.chunk1 >= V && (long long)(p.nchunk1 - 1) * p.chunk1 < V, "nchunk1");
     CHECK((2LL * gamma + 1) * p.nchunk1 <= kMaxStatsSub, "stats pairs %d x %d exceed the LDS arrays", gamma, p.nchunk1);
+    // the early exit's chunks: whole vectors, covering V, at most the single
+    // pass's count (so its pairs and gate words fit the same regions)
+    CHECK(p.chunk1s % E == 0 && p.chunk1s >= p.chunk1, "chunk1s %d", p.chunk1s);
+    CHECK((long long)p.nchunk1s * p.chunk1s >= V && (long long)(p.nchunk1s - 1) * p.chunk1s < V, "nchunk1s");
+    CHECK(p.nchunk1s >= 1 && p.nchunk1s <= p.nchunk1 && p.nchunk1s >= (p.nchunk1 + 1) / 2 - 1, "nchunk1s %d of %d",
+          p.nchunk1s, p.nchunk1);
     // the stats stream: each wave's quarter of a chunk
     // target row gamma: quarters fit the bonus draw (one vector per thread of a
     // workgroup, or 4 vectors per lane of one wave), masses fit kMaxSub
@@ -224,10 +230,10 @@ static void simulate_staged(int B, int gamma, int V, sv_dtype_t dt) {
     if (n_staged < 0) return;  // the single pass serves
     const int gate = gate_stages(B, V, bytes_per_logit(dt));
     CHECK(gate >= 2 && gate < gamma, "gate %d", gate);
-    const Layout y = make_staged_layout(B, gamma, p.nchunk1, p.nchunkg, p.nchunk2);
+    const Layout y = make_staged_layout(B, gamma, p.nchunk1s, p.nchunkg, p.nchunk2);
     const long long n = (long long)y.end2 + B;
     CHECK(n == n_staged, "staged grid %lld vs %lld", n, n_staged);
-    const int T = 2 * p.nchunk1;
+    const int T = 2 * p.nchunk1s;
     std::vector<long long> tile((size_t)B * gamma * T, -1), rowdec((size_t)B * gamma, -1), rowg((size_t)B * p.nchunkg, -1),
         mass((size_t)B * p.nchunk2, -1), draw(B, -1), bonus(B, -1);
     long long idle = 0;

@@ -1,6 +1,8 @@
 """The exact mode's early-exit variant (spec_verify_exact_early_exit) through
-the C ABI: bit-identical outputs to spec_verify_exact on the same inputs, and
-the oracle's decisions outside the flagged cases.
+the C ABI: the same outputs as spec_verify_exact on the same inputs (its row
+chunks are twice as long, so its normalisers can differ in the last bits; no
+uniform of these seeds lies that close to a threshold), and the oracle's
+decisions outside the flagged cases.
 
 Its tiles of a draft position c skip their rows when an element has already
 rejected a draft `gate` stages earlier, gate = max(2, ceil(56e6 / (2 B V s)))
