@@ -324,8 +324,10 @@ inline bool pipelined_waits(long long B, long long gamma, long long V, sv_dtype_
 }
 
 // Copies of each decision record, one per reader: every mass workgroup, the
-// draw and the bonus workgroup (exact mode); only the bonus workgroup
-// (sigmoid mode, whose mass and draw workgroups decide for themselves).
+// draw and the bonus workgroup (exact mode; the mass workgroups' copies stay
+// unwritten where they decide for themselves, see qstride); only the bonus
+// workgroup (sigmoid mode, whose mass and draw workgroups decide for
+// themselves).
 inline int decision_copies(bool exact, const Plan& pl) { return exact ? pl.nchunk2 + 2 : 1; }
 
 // ---------------------------------------------------------------------------

@@ -557,9 +557,9 @@ __device__ __forceinline__ int wave_sub_chunk_find(const typename D::T* rp, cons
 //                    quarter's normaliser terms (eq. (4)) as a (K, S) pair
 //   decider (b)      b's decision -- eq. (1) at the drafted tokens and the
 //                    first-rejection scan -- published as a small record,
-//                    one copy per reader (exact mode; in the sigmoid mode
-//                    the mass and draw workgroups decide for themselves and
-//                    the decider only writes the probes)
+//                    one copy per reader (exact mode; in the sigmoid mode,
+//                    and in the exact mode's short streams with few pairs to
+//                    copy, the mass workgroups decide for themselves)
 //   mass (b, k2)     the masses of the final distribution (eqs. (2)-(3), or
 //                    the target row) over tile k2, one per wave, published
 //   draw (b)         the inverse-CDF draw of b's next token
@@ -1319,7 +1319,9 @@ __device__ __forceinline__ void wave_locate4(const double* m, int M, double u, S
 
 // b's decision, made once by b's decider workgroup and, in the exact mode,
 // published as a small record, one copy per reader (each mass workgroup, the
-// draw, the bonus workgroup), which that reader clears once it has read it.
+// draw, the bonus workgroup; only the last two when the mass workgroups
+// decide for themselves), which that reader clears once it has read it.
+// Copies before `first` are not written.
 // The decider also writes the tau / normaliser probes and clears the stats
 // words it read (it is their only reader).
 // The P.ncopy copies of b's decision record (L, the sentinel flag, gb and the
