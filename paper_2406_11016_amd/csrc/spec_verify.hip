@@ -808,8 +808,9 @@ __device__ __forceinline__ void stats_role(const StepParams& P, int b, int slot,
         return;
     }
     if constexpr (kPipe) {
-        // short streams: the pair goes to b's decider and to each of b's mass
-        // workgroups (which decide for themselves), one copy per thread
+        // short streams: the pair goes to b's decider and, where b's mass
+        // workgroups decide for themselves (qstride > 0), to each of them,
+        // one copy per thread
         const Lse t = block_lse_all(st, sm.sk, sm.ss);
         const size_t at = ((size_t)slot * P.nchunk1 + k) * 2;
         const int ncp = (P.qstride > 0) ? P.nchunk2 : 0;
