@@ -982,6 +982,104 @@ __device__ __forceinline__ void merge_rows(Smem& sm, int R, int W, int Rg = 0) {
     __syncthreads();
 }
 
+// The short streams' wait for the R decision rows' pairs at p (W per row)
+// and their merge into sm.rowL, with no LDS staging: thread (i, g) of the
+// merge (row i = tid / G, lane g of the row's group of G, G as in
+// merge_rows) polls the words of its own pairs g, g + G, g + 2G, g + 3G
+// directly (two polls in flight), the workgroup agrees through LDS flags
+// that every pair is in, and the merge then runs on the registers: the same
+// values, order and group butterfly as merge_rows<true>, so the same bits.
+// Needs W <= 4 G (the caller checks).  Ends with a workgroup barrier.
+__device__ __forceinline__ bool wait_merge_rows(const unsigned long long* p, int R, int W, Smem& sm, int limit) {
+    constexpr int kB = 4;
+    const int G = (R <= 16) ? 16 : (R <= 32) ? 8 : (R <= 64) ? 4 : (R <= 128) ? 2 : 1;
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int i = tid / G, g = tid % G;
+    const int nu = (W + G - 1) / G;  // pairs per lane (uniform)
+    const bool row = i < R;
+    const int ic = min(i, R - 1);
+    bool have[kB];
+    const unsigned long long* q[kB];
+#pragma unroll
+    for (int u = 0; u < kB; ++u) {
+        const int j = g + u * G;
+        have[u] = row && j < W;
+        q[u] = p + 2 * ((size_t)ic * W + min(j, W - 1));
+    }
+    __shared__ int mflag[2][kWaves];
+    unsigned long long a[2 * kB], c[2 * kB];
+    auto issue = [&](unsigned long long (&w)[2 * kB]) {
+#pragma unroll
+        for (int u = 0; u < kB; ++u) {
+            if (u < nu) {
+                w[2 * u] = __hip_atomic_load(q[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                w[2 * u + 1] = __hip_atomic_load(q[u] + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+                w[2 * u] = w[2 * u + 1] = 0ull;
+            }
+        }
+    };
+    auto check = [&](const unsigned long long (&w)[2 * kB], int round) {
+        bool missing = false;
+#pragma unroll
+        for (int u = 0; u < kB; ++u) missing |= have[u] && (w[2 * u] == 0ull || w[2 * u + 1] == 0ull);
+        const unsigned long long m = __ballot(missing);
+        if (lane == 0) mflag[round & 1][wave] = (m != 0ull) ? 1 : 0;
+        lds_barrier();
+        int any = 0;
+#pragma unroll
+        for (int w2 = 0; w2 < kWaves; ++w2) any |= mflag[round & 1][w2];
+        return any == 0;
+    };
+    unsigned long long w[2 * kB];
+    bool ok = false;
+    issue(a);
+    for (int round = 0;; round += 2) {
+        issue(c);
+        if (check(a, round)) {
+#pragma unroll
+            for (int k = 0; k < 2 * kB; ++k) w[k] = a[k];
+            ok = true;
+            break;
+        }
+        if (round + 1 >= limit) break;
+        issue(a);
+        if (check(c, round + 1)) {
+#pragma unroll
+            for (int k = 0; k < 2 * kB; ++k) w[k] = c[k];
+            ok = true;
+            break;
+        }
+        if (round + 2 >= limit) break;
+    }
+    if (!ok) {
+#pragma unroll
+        for (int k = 0; k < 2 * kB; ++k) w[k] = 0ull;  // decodes as a NaN pair: the caller reports the timeout
+    }
+    float kb[kB];
+    double sb[kB];
+#pragma unroll
+    for (int u = 0; u < kB; ++u) {
+        kb[u] = have[u] ? (float)decode_word(w[2 * u]) : -INFINITY;
+        sb[u] = have[u] ? decode_word(w[2 * u + 1]) : 0.0;
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kB; ++u) m = fmaxf(m, kb[u]);
+    m = group_max(m, G);
+    double sum = 0.0;
+#pragma unroll
+    for (int u = 0; u < kB; ++u)
+        if (have[u]) sum += ldexp(sb[u], exp_delta(kb[u] - m));
+    sum = group_sum(sum, G);
+    if (row && g == 0)
+        sm.rowL[i] = (sum != sum) ? __builtin_nan("")
+                     : ((m == -INFINITY) ? -INFINITY
+                                         : (double)m + ((sum > 0.0 && sum < INFINITY) ? log2_pos_fast(sum) : log2(sum)));
+    __syncthreads();
+    return ok;
+}
+
 // For the drafts c < gamma (thread c holds stop_c: 0 accepted, 1 rejected, 2
 // unreadable, and tok_ok): the first c with stop_c != 0 (kThreads if none),
 // whether that one is unreadable, and whether any drafted token is out of
@@ -1078,9 +1176,15 @@ __device__ __forceinline__ Decision decide(const StepParams& P, int b, Smem& sm,
         // the stats slots the decision reads, merged into log2-normalisers
         // max K + log2(sum S 2^(K - max K)) by exact power-of-two scaling
         const int W = P.nchunk1;  // chunks per row
-        d.ok = wait_ks<kPipe>((ks != nullptr) ? ks : P.pslot + (size_t)b * P.pstride, 2 * gamma * W, sm.K, sm.S,
-                              spin_limit(P));
-        merge_rows<kPipe>(sm, 2 * gamma, W);
+        unsigned long long* src = (ks != nullptr) ? ks : P.pslot + (size_t)b * P.pstride;
+        const int R = 2 * gamma;
+        const int G = (R <= 16) ? 16 : (R <= 32) ? 8 : (R <= 64) ? 4 : (R <= 128) ? 2 : 1;
+        if (kPipe && W <= 4 * G) {
+            d.ok = wait_merge_rows(src, R, W, sm, spin_limit(P));
+        } else {
+            d.ok = wait_ks<kPipe>(src, R * W, sm.K, sm.S, spin_limit(P));
+            merge_rows<kPipe>(sm, R, W);
+        }
     }
 
     int stop = 0;
